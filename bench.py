@@ -1,0 +1,229 @@
+"""Benchmark of the SSBA forward path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload grid64]
+                    [--no-cpu] [--sweep]
+
+One step = one SSBA layer call on inputs already resident in HBM: the top-k
+gate (block pooling, affinity, ranking -> index) followed by the block-sparse
+attention kernel.  Prints ONE JSON line on stdout; --sweep prints extra
+per-configuration lines on stderr (sparsity sweep, text tokens, 2K grid).
+
+Flops are counted over computed (kept) query/key pairs only: 4 * D per pair
+(2 * D for Q K^T, 2 * D for P V).  Pairs per (batch, head):
+T_img * (keep * Bt^2 + T_txt) + T_txt * T.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def pairs_per_bh(w, keep=None) -> int:
+    keep = w.keep if keep is None else keep
+    if w.gate == "window":
+        keep = w.window[0] * w.window[1]
+    elif w.gate == "dense":
+        keep = w.n_tiles
+    return w.t_img * (keep * w.tile * w.tile + w.n_text) + w.n_text * w.seq_len
+
+
+def flops(w, dense=False) -> float:
+    pairs = w.seq_len * w.seq_len if dense else pairs_per_bh(w)
+    return 4.0 * w.head_dim * pairs * w.batch * w.heads
+
+
+def describe(w) -> str:
+    s = f"B{w.batch} H{w.heads} {w.grid_h}x{w.grid_w} tokens D{w.head_dim} {w.tile}x{w.tile} blocks"
+    if w.gate == "topk":
+        s += f" top-k keep {w.keep}/{w.n_tiles} ({100 * (1 - w.keep / w.n_tiles):.3f}% masked)"
+    elif w.gate == "window":
+        s += f" window {w.window[0]}x{w.window[1]} blocks"
+    else:
+        s += " dense gate"
+    if w.n_text:
+        s += f" + {w.n_text} dense text tokens"
+    return s + f" shift {w.shift} bf16 seed {w.seed}"
+
+
+class Runner:
+    """Preallocated buffers and the timed calls of one workload."""
+
+    def __init__(self, w):
+        import torch
+        from paper_2605_15684_amd import ssba
+        from paper_2605_15684_amd.inputs import make_qkv
+        self.torch, self.ssba, self.w = torch, ssba, w
+        self.q, self.k, self.v = make_qkv(w, device="cuda")
+        self.desc = ssba.desc_for(self.q, grid=(w.grid_h, w.grid_w), tile=w.tile, shift=w.shift,
+                                  n_text=w.n_text, gate=w.gate, keep=w.keep, window=w.window)
+        self.index, self.scratch = ssba.alloc_workspace(self.desc, self.q.device)
+        self.out = torch.empty_like(self.q)
+        self.out_dense = torch.empty_like(self.q)
+
+    def step(self):
+        self.ssba.build_index(self.q, self.k, self.desc, self.index, self.scratch)
+        self.ssba.forward(self.q, self.k, self.v, self.index, self.desc, self.out)
+
+    def timed_steps(self, steps: int):
+        """Events around each launch of `steps` back-to-back steps."""
+        torch = self.torch
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for e in ev:
+            e[0].record()
+            self.ssba.build_index(self.q, self.k, self.desc, self.index, self.scratch)
+            e[1].record()
+            self.ssba.forward(self.q, self.k, self.v, self.index, self.desc, self.out)
+            e[2].record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        idx_ms = [e[0].elapsed_time(e[1]) for e in ev]
+        fwd_ms = [e[1].elapsed_time(e[2]) for e in ev]
+        span_ms = ev[0][0].elapsed_time(ev[-1][2])
+        return wall * 1e3 / steps, span_ms / steps, float(np.mean(idx_ms)), float(np.mean(fwd_ms))
+
+    def timed_dense(self, steps: int) -> float:
+        torch = self.torch
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for _ in range(3):
+            self.ssba.forward_dense(self.q, self.k, self.v, self.desc, self.out_dense)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(steps):
+            self.ssba.forward_dense(self.q, self.k, self.v, self.desc, self.out_dense)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+
+def cpu_baseline(runner, budget_s: float = 12.0) -> dict:
+    """The fp64 oracle on the same inputs: the gate for every (batch, head),
+    then attention head by head until the time budget is spent."""
+    import torch
+    from oracle import ssba_oracle as O
+    w = runner.w
+    q = runner.q.double().cpu().numpy()
+    k = runner.k.double().cpu().numpy()
+    v = runner.v.double().cpu().numpy()
+    kw = dict(grid_h=w.grid_h, grid_w=w.grid_w, tile=w.tile, shift=w.shift, n_text=w.n_text)
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    t0 = time.perf_counter()
+    idx = O.build_index(q, k, gate=w.gate, keep=w.keep, window=w.window, **kw)
+    t_index = time.perf_counter() - t0
+    n_bh = w.batch * w.heads
+    done, t_attn = 0, 0.0
+    for bh in range(n_bh):
+        b, h = divmod(bh, w.heads)
+        t1 = time.perf_counter()
+        O.attention(q, k, v, idx, heads=[(b, h)], **kw)
+        t_attn += time.perf_counter() - t1
+        done += 1
+        if t_index + t_attn > budget_s:
+            break
+    per_bh = flops(w) / n_bh
+    sec = t_index * done / n_bh + t_attn
+    return {"value": per_bh * done / sec / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"fp64 oracle: gate for all {n_bh} (batch, head) pairs "
+                      f"({t_index:.2f} s, pro-rated), attention for {done} of {n_bh} pairs "
+                      f"({t_attn:.2f} s); host {platform.processor() or platform.machine()}, "
+                      f"os.cpu_count()={os.cpu_count()}",
+            "seconds": round(t_index + t_attn, 3)}
+
+
+def measure(w, steps: int, warmup: int, dense_steps: int):
+    r = Runner(w)
+    for _ in range(warmup):
+        r.step()
+    wall_ms, step_ms, idx_ms, fwd_ms = r.timed_steps(steps)
+    dense_ms = r.timed_dense(dense_steps)
+    f = flops(w)
+    return r, {
+        "ms_step_wall": wall_ms, "ms_step": step_ms, "ms_index": idx_ms, "ms_fwd": fwd_ms,
+        "ms_dense": dense_ms, "gflop": f / 1e9, "gflop_dense": flops(w, dense=True) / 1e9,
+        "tflops_fwd": f / (fwd_ms * 1e-3) / 1e12,
+        "tflops_step": f / (step_ms * 1e-3) / 1e12,
+        "tflops_dense": flops(w, dense=True) / (dense_ms * 1e-3) / 1e12,
+        "speedup_kernel": dense_ms / fwd_ms, "speedup_step": dense_ms / step_ms,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="grid64")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--sweep", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the SSBA path has no multi-GPU mode in this build "
+              "(heads and batch shard with no exchange; see the design notes).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2605_15684_amd.inputs import SWEEP_TOPK_KEEP, SWEEP_WINDOW, preset
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+
+    w = preset(args.workload)
+    r, m = measure(w, args.steps, args.warmup, max(20, args.steps // 4))
+    f = flops(w)
+    achieved = f / (m["ms_fwd"] * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "kernel": "k_attn_bf16", "achieved": round(achieved, 2),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "traffic": None}
+    cpu = None if args.no_cpu else cpu_baseline(r)
+    line = {
+        "metric": "SSBA fwd ms/call + effective TFLOP/s (% bf16 MFMA peak) at 4096 tokens, 84% sparse",
+        "value": round(m["tflops_step"], 2), "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(m["ms_step"], 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{w.name}: {describe(w)}", "global_batch": w.batch,
+                   "seq_len": w.seq_len, "parallelism": "none (1 GPU)"},
+        "ms_fwd": round(m["ms_fwd"], 5), "ms_index": round(m["ms_index"], 5),
+        "ms_dense": round(m["ms_dense"], 5), "ms_step_wall": round(m["ms_step_wall"], 5),
+        "tflops_fwd": round(m["tflops_fwd"], 2), "pct_peak_fwd": round(100 * m["tflops_fwd"] / PEAK_BF16_TFLOPS, 2),
+        "tflops_dense": round(m["tflops_dense"], 2),
+        "speedup_vs_dense_kernel": round(m["speedup_kernel"], 3),
+        "speedup_vs_dense_step": round(m["speedup_step"], 3),
+        "gflop_computed": round(m["gflop"], 3), "gflop_dense": round(m["gflop_dense"], 3),
+        "roofline": roofline, "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+    if args.sweep:
+        cases = [preset("sweep64", keep=kp) for kp in SWEEP_TOPK_KEEP.values()]
+        cases += [preset("sweep64", gate="window", window=wd) for wd in SWEEP_WINDOW.values()]
+        cases += [preset("grid64_text"), preset("grid128")]
+        for c in cases:
+            del r
+            torch.cuda.empty_cache()
+            r, mm = measure(c, max(20, args.steps // 2), 5, 20)
+            print(json.dumps({"workload": c.name, "desc": describe(c),
+                              **{k: round(v, 5) for k, v in mm.items()},
+                              "pct_peak_fwd": round(100 * mm["tflops_fwd"] / PEAK_BF16_TFLOPS, 2)}),
+                  file=sys.stderr, flush=True)
+
+
+if __name__ == "__main__":
+    main()

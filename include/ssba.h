@@ -1,0 +1,137 @@
+/*
+ * ssba.h -- C ABI of the Shift Sparse Block Attention (SSBA) forward pass for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * SSBA (ElasticDiT, Section 2.2) is masked softmax attention over a diffusion
+ * transformer's [text; image] token sequence.  The image tokens form an
+ * H_g x W_g grid.  Per layer the grid origin is shifted by Delta (Section
+ * 2.2.2, torch.roll semantics) and cut into Bt x Bt blocks.  Each image query
+ * block keeps a subset of image key blocks (the gate).  Text tokens see
+ * everything and are seen by everything (Algorithm 1, pad step).
+ *
+ * Gates (all three emit the same index layout, consumed by ssba_forward):
+ *   SSBA_GATE_TOPK   -- Section 2.2.1 "Block Compression", "Affinity Matrix",
+ *                       "Top-k Gating" (Eq. 1; Algorithm 1, pool/affinity/
+ *                       top-k steps): per-block pooled Q and K, S = q_b k_b^T,
+ *                       keep the `keep` largest entries of each row of S
+ *                       (i.e. drop the floor(T_b * rho) smallest); ties keep
+ *                       the lower key-block index; +0 == -0; NaN ranks last.
+ *                       Pooled values are sums (mean x Bt^2), in fp64, added
+ *                       in slot order; S is summed over channels in order,
+ *                       without fused multiply-add.  Lists are therefore
+ *                       bit-reproducible.
+ *   SSBA_GATE_WINDOW -- control gate: block i sees block j iff both lie in one
+ *                       win_h x win_w window of blocks of the shifted frame.
+ *   SSBA_GATE_DENSE  -- every block sees every block (zero sparsity).
+ *
+ * Sequence layout: T = n_text + grid_h * grid_w rows; text rows first; image
+ * row n_text + y * grid_w + x holds grid token (y, x).  Q, K, V and O share one
+ * element-stride triple (stride_b, stride_h, stride_t); the channel stride is 1.
+ * Passing all three strides as 0 selects the contiguous [B, H, T, D] layout.
+ *
+ * Shifted frame: with (sy, sx) reduced mod (grid_h, grid_w), block t =
+ * (ty, tx) (row-major over the n_y x n_x block grid) and slot s (row-major
+ * inside the block) hold the image token at
+ *   y = (ty * Bt + s / Bt - sy) mod grid_h,   x = (tx * Bt + s % Bt - sx) mod grid_w.
+ * The shift is applied through this address map: no data is moved.
+ *
+ * Ownership and threading: the caller allocates and owns every buffer (device
+ * memory, e.g. torch tensors).  The library allocates no device memory, keeps
+ * no per-call state and may be called from several host threads.  Every call
+ * is asynchronous on the caller's HIP stream (`hip_stream` = hipStream_t, NULL
+ * for the null stream); only ssba_read_device_status synchronizes.
+ *
+ * Errors: descriptor and pointer checks happen before anything is launched;
+ * on a non-zero status nothing has been enqueued and outputs are untouched.
+ * SSBA_ERR_HIP reports a failed launch (hipGetLastError).
+ */
+#ifndef SSBA_H_
+#define SSBA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SSBA_ABI_VERSION 1
+
+typedef enum {
+  SSBA_OK = 0,
+  SSBA_ERR_ARG = 1,          /* null pointer, bad enum, bad keep / window   */
+  SSBA_ERR_SHAPE = 2,        /* non-positive sizes, grid not a multiple of Bt */
+  SSBA_ERR_UNSUPPORTED = 3,  /* head_dim / tile / block count not built     */
+  SSBA_ERR_WORKSPACE = 4,    /* (reserved)                                  */
+  SSBA_ERR_NONFINITE = 5,    /* gate saw a NaN/Inf affinity (device status) */
+  SSBA_ERR_HIP = 6           /* HIP launch or copy failure                  */
+} ssba_status;
+
+typedef enum { SSBA_DT_BF16 = 0, SSBA_DT_F32 = 1 } ssba_dtype;
+typedef enum { SSBA_GATE_TOPK = 0, SSBA_GATE_WINDOW = 1, SSBA_GATE_DENSE = 2 } ssba_gate;
+
+typedef struct ssba_desc {
+  int32_t batch, heads, head_dim;  /* B >= 1, H >= 1, D in {64, 128}               */
+  int32_t grid_h, grid_w, tile;    /* Bt in {4, 8, 16}; grid_h, grid_w multiples of Bt */
+  int32_t shift_y, shift_x;        /* Delta, any sign, reduced mod the grid          */
+  int32_t n_text;                  /* >= 0 text tokens, stored before the image rows */
+  int32_t gate;                    /* ssba_gate                                      */
+  int32_t keep;                    /* TOPK: kept key blocks per query block, 1..T_b  */
+  int32_t win_h, win_w;            /* WINDOW: window in blocks; n_y % win_h == n_x % win_w == 0 */
+  int32_t dtype;                   /* ssba_dtype of Q, K, V and O                    */
+  float softmax_scale;             /* <= 0 selects 1 / sqrt(head_dim)                */
+  int64_t stride_b, stride_h, stride_t; /* element strides; all 0 = contiguous     */
+} ssba_desc;
+
+/* Returns SSBA_ABI_VERSION. */
+int ssba_abi_version(void);
+
+/* Static, never-NULL description of a status code. */
+const char* ssba_status_str(ssba_status s);
+
+/* Device bytes the caller must provide.
+ *   index_bytes   = 4 * B * H * T_b * (1 + T_b): the index of ssba_build_index.
+ *   scratch_bytes = TOPK: 16 * B * H * T_b * D (fp64 pooled q_b and k_b)
+ *                   + 4 * B * H * T_b (per-row status flags);
+ *                   WINDOW / DENSE: 4 * B * H * T_b.
+ * Either output pointer may be NULL.  T_b = grid_h * grid_w / Bt^2. */
+ssba_status ssba_workspace_size(const ssba_desc* d, size_t* index_bytes, size_t* scratch_bytes);
+
+/* Gate (Section 2.2.1 Block Compression / Affinity / Top-k Gating; Algorithm 1
+ * pool, affinity, top-k and expand steps).  Writes `index`, int32
+ * [B][H][T_b][1 + T_b]: entry 0 = count of kept key blocks, then their block
+ * ids ascending, then -1 padding.  TOPK reads the image rows of q and k (dtype
+ * d->dtype, layout above); WINDOW and DENSE read neither (q, k may be NULL).
+ * `scratch` (scratch_bytes, any alignment >= 8) is overwritten; its status
+ * flags are read by ssba_read_device_status. */
+ssba_status ssba_build_index(const ssba_desc* d, const void* q, const void* k,
+                             int32_t* index, void* scratch, void* hip_stream);
+
+/* SSBA attention (Algorithm 1, attend step): O = softmax(scale * Q K^T + mask) V
+ * where an image query in block i sees the image keys of the blocks listed in
+ * index[b][h][i] and every text key; a text query sees every key.  Masked
+ * blocks are never loaded.  Writes all T rows of o (text rows included);
+ * the image rows are the layer output of Algorithm 1's return step.
+ * bf16: products and accumulation in fp32 (MFMA), probabilities rounded to
+ * bf16 before the value product, output rounded to bf16.  f32: fp32 throughout.
+ * `index` must come from ssba_build_index with the same grid/tile/shift
+ * (counts in 0..T_b, ids in 0..T_b-1; other contents are undefined behaviour). */
+ssba_status ssba_forward(const ssba_desc* d, const void* q, const void* k, const void* v,
+                         const int32_t* index, void* o, void* hip_stream);
+
+/* Dense attention in the same kernel family (the zero-sparsity control of
+ * Section 2.2.1's cost comparison): every query sees all T keys; the gate,
+ * shift and index are ignored. */
+ssba_status ssba_forward_dense(const ssba_desc* d, const void* q, const void* k, const void* v,
+                               void* o, void* hip_stream);
+
+/* Synchronizes `hip_stream`, then reads the status flags that the last
+ * ssba_build_index left in `scratch` (same descriptor): SSBA_OK, or
+ * SSBA_ERR_NONFINITE if any affinity row held a NaN or Inf (TOPK only). */
+ssba_status ssba_read_device_status(const ssba_desc* d, const void* scratch, ssba_status* out,
+                                    void* hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SSBA_H_ */

@@ -1,0 +1,114 @@
+"""ctypes view of libssba.so (include/ssba.h).  Argument marshalling only.
+
+Loading fails loudly (ImportError) when the library has not been built: there
+is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libssba.so")
+
+SSBA_OK = 0
+SSBA_ERR_ARG = 1
+SSBA_ERR_SHAPE = 2
+SSBA_ERR_UNSUPPORTED = 3
+SSBA_ERR_WORKSPACE = 4
+SSBA_ERR_NONFINITE = 5
+SSBA_ERR_HIP = 6
+
+DT_BF16 = 0
+DT_F32 = 1
+GATE_TOPK = 0
+GATE_WINDOW = 1
+GATE_DENSE = 2
+
+EXPORTS = ("ssba_abi_version", "ssba_status_str", "ssba_workspace_size", "ssba_build_index",
+           "ssba_forward", "ssba_forward_dense", "ssba_read_device_status")
+
+
+class SsbaDesc(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32), ("heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+        ("grid_h", ctypes.c_int32), ("grid_w", ctypes.c_int32), ("tile", ctypes.c_int32),
+        ("shift_y", ctypes.c_int32), ("shift_x", ctypes.c_int32),
+        ("n_text", ctypes.c_int32), ("gate", ctypes.c_int32), ("keep", ctypes.c_int32),
+        ("win_h", ctypes.c_int32), ("win_w", ctypes.c_int32), ("dtype", ctypes.c_int32),
+        ("softmax_scale", ctypes.c_float),
+        ("stride_b", ctypes.c_int64), ("stride_h", ctypes.c_int64), ("stride_t", ctypes.c_int64),
+    ]
+
+
+class SsbaError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_str(status)} (status {status})")
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libssba.so once.  Raises ImportError if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is not built; run `python -m paper_2605_15684_amd.build` "
+                          "(the SSBA path has no CPU fallback)")
+    lib = ctypes.CDLL(path)
+    vp, sz = ctypes.c_void_p, ctypes.c_size_t
+    dp = ctypes.POINTER(SsbaDesc)
+    lib.ssba_abi_version.restype = ctypes.c_int
+    lib.ssba_abi_version.argtypes = []
+    lib.ssba_status_str.restype = ctypes.c_char_p
+    lib.ssba_status_str.argtypes = [ctypes.c_int]
+    lib.ssba_workspace_size.restype = ctypes.c_int
+    lib.ssba_workspace_size.argtypes = [dp, ctypes.POINTER(sz), ctypes.POINTER(sz)]
+    lib.ssba_build_index.restype = ctypes.c_int
+    lib.ssba_build_index.argtypes = [dp, vp, vp, vp, vp, vp]
+    lib.ssba_forward.restype = ctypes.c_int
+    lib.ssba_forward.argtypes = [dp, vp, vp, vp, vp, vp, vp]
+    lib.ssba_forward_dense.restype = ctypes.c_int
+    lib.ssba_forward_dense.argtypes = [dp, vp, vp, vp, vp, vp]
+    lib.ssba_read_device_status.restype = ctypes.c_int
+    lib.ssba_read_device_status.argtypes = [dp, vp, ctypes.POINTER(ctypes.c_int), vp]
+    _lib = lib
+    return lib
+
+
+def status_str(status: int) -> str:
+    return load().ssba_status_str(int(status)).decode()
+
+
+def check(status: int, where: str) -> None:
+    if status != SSBA_OK:
+        raise SsbaError(status, where)
+
+
+def workspace_size(desc: SsbaDesc):
+    ib, sb = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    check(load().ssba_workspace_size(ctypes.byref(desc), ctypes.byref(ib), ctypes.byref(sb)),
+          "ssba_workspace_size")
+    return ib.value, sb.value
+
+
+def build_index(desc, q_ptr, k_ptr, index_ptr, scratch_ptr, stream) -> int:
+    return load().ssba_build_index(ctypes.byref(desc), q_ptr, k_ptr, index_ptr, scratch_ptr, stream)
+
+
+def forward(desc, q_ptr, k_ptr, v_ptr, index_ptr, o_ptr, stream) -> int:
+    return load().ssba_forward(ctypes.byref(desc), q_ptr, k_ptr, v_ptr, index_ptr, o_ptr, stream)
+
+
+def forward_dense(desc, q_ptr, k_ptr, v_ptr, o_ptr, stream) -> int:
+    return load().ssba_forward_dense(ctypes.byref(desc), q_ptr, k_ptr, v_ptr, o_ptr, stream)
+
+
+def read_device_status(desc, scratch_ptr, stream):
+    out = ctypes.c_int(0)
+    check(load().ssba_read_device_status(ctypes.byref(desc), scratch_ptr, ctypes.byref(out), stream),
+          "ssba_read_device_status")
+    return out.value

@@ -1,0 +1,249 @@
+// C ABI of the SSBA forward library: argument validation, workspace sizing and
+// dispatch to the gfx950 kernels.  See include/ssba.h for the contract.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+#include "ssba.h"
+#include "ssba_common.h"
+
+namespace {
+
+using ssba::AttnArgs;
+using ssba::Frame;
+using ssba::IndexArgs;
+
+constexpr int kMaxTiles = 1024;  // one gate workgroup ranks a whole row
+
+int ilog2(int v) {
+  int l = 0;
+  while ((1 << l) < v) ++l;
+  return l;
+}
+
+int mod(int a, int m) {
+  const int r = a % m;
+  return r < 0 ? r + m : r;
+}
+
+struct Shape {
+  int64_t sb, sh, st;
+  int n_tiles, ny, nx, seq;
+  Frame f;
+};
+
+// Structural checks shared by every entry point (no pointers).  The dense
+// path ignores the gate fields (gate, keep, window).
+ssba_status check_desc(const ssba_desc* d, Shape* out, bool gate_fields = true) {
+  if (!d) return SSBA_ERR_ARG;
+  if (d->batch < 1 || d->heads < 1 || d->grid_h < 1 || d->grid_w < 1 || d->n_text < 0)
+    return SSBA_ERR_SHAPE;
+  if (d->dtype != SSBA_DT_BF16 && d->dtype != SSBA_DT_F32) return SSBA_ERR_ARG;
+  if (gate_fields && d->gate != SSBA_GATE_TOPK && d->gate != SSBA_GATE_WINDOW &&
+      d->gate != SSBA_GATE_DENSE)
+    return SSBA_ERR_ARG;
+  if (d->head_dim != 64 && d->head_dim != 128) return SSBA_ERR_UNSUPPORTED;
+  if (d->tile != 4 && d->tile != 8 && d->tile != 16) return SSBA_ERR_UNSUPPORTED;
+  if (d->grid_h % d->tile || d->grid_w % d->tile) return SSBA_ERR_SHAPE;
+  if (!(std::isfinite(d->softmax_scale))) return SSBA_ERR_ARG;
+  const int64_t t_img = (int64_t)d->grid_h * d->grid_w;
+  const int64_t seq = d->n_text + t_img;
+  if (seq > (int64_t)1 << 30) return SSBA_ERR_UNSUPPORTED;
+  const int64_t n_tiles = t_img / ((int64_t)d->tile * d->tile);
+  if (n_tiles > kMaxTiles) return SSBA_ERR_UNSUPPORTED;
+  const int ny = d->grid_h / d->tile, nx = d->grid_w / d->tile;
+  if (gate_fields && d->gate == SSBA_GATE_TOPK && (d->keep < 1 || d->keep > n_tiles))
+    return SSBA_ERR_ARG;
+  if (gate_fields && d->gate == SSBA_GATE_WINDOW &&
+      (d->win_h < 1 || d->win_w < 1 || ny % d->win_h || nx % d->win_w))
+    return SSBA_ERR_ARG;
+  int64_t sb = d->stride_b, sh = d->stride_h, st = d->stride_t;
+  if (sb == 0 && sh == 0 && st == 0) {
+    st = d->head_dim;
+    sh = seq * st;
+    sb = (int64_t)d->heads * sh;
+  } else if (sb < 1 || sh < 1 || st < d->head_dim) {
+    return SSBA_ERR_SHAPE;
+  }
+  // 16-byte vector loads in the bf16 kernel need 8-element aligned rows.
+  if (d->dtype == SSBA_DT_BF16 && ((sb | sh | st) & 7)) return SSBA_ERR_UNSUPPORTED;
+  // Element offsets must stay inside int64 and row indices inside int32.
+  const double span = (double)(d->batch - 1) * sb + (double)(d->heads - 1) * sh + (double)seq * st;
+  if (span > 9.0e18) return SSBA_ERR_SHAPE;
+  if (out) {
+    out->sb = sb;
+    out->sh = sh;
+    out->st = st;
+    out->n_tiles = (int)n_tiles;
+    out->ny = ny;
+    out->nx = nx;
+    out->seq = (int)seq;
+    out->f.grid_h = d->grid_h;
+    out->f.grid_w = d->grid_w;
+    out->f.tile_log2 = ilog2(d->tile);
+    out->f.nx = nx;
+    out->f.sy = mod(d->shift_y, d->grid_h);
+    out->f.sx = mod(d->shift_x, d->grid_w);
+    out->f.n_text = d->n_text;
+  }
+  return SSBA_OK;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+size_t index_bytes_of(const ssba_desc* d, const Shape& s) {
+  return (size_t)4 * d->batch * d->heads * s.n_tiles * (s.n_tiles + 1);
+}
+
+size_t scratch_bytes_of(const ssba_desc* d, const Shape& s) {
+  const size_t flags = (size_t)4 * d->batch * d->heads * s.n_tiles;
+  if (d->gate == SSBA_GATE_TOPK)
+    return (size_t)16 * d->batch * d->heads * s.n_tiles * d->head_dim + flags;
+  return flags;
+}
+
+AttnArgs attn_args(const ssba_desc* d, const Shape& s, const void* q, const void* k, const void* v,
+                   const int32_t* index, void* o, bool dense) {
+  AttnArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.o = o;
+  a.index = index;
+  a.sb = s.sb;
+  a.sh = s.sh;
+  a.st = s.st;
+  a.batch = d->batch;
+  a.heads = d->heads;
+  a.seq = s.seq;
+  a.n_tiles = s.n_tiles;
+  a.f = s.f;
+  const float scale = d->softmax_scale > 0.f ? d->softmax_scale : 1.0f / std::sqrt((float)d->head_dim);
+  a.scale = scale;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.dense = dense ? 1 : 0;
+  return a;
+}
+
+ssba_status run_attention(const ssba_desc* d, const void* q, const void* k, const void* v,
+                          const int32_t* index, void* o, void* stream, bool dense) {
+  Shape s;
+  ssba_status st = check_desc(d, &s, !dense);
+  if (st != SSBA_OK) return st;
+  if (!q || !k || !v || !o || (!dense && !index)) return SSBA_ERR_ARG;
+  const size_t al = d->dtype == SSBA_DT_BF16 ? 16 : 4;
+  if (!aligned(q, al) || !aligned(k, al) || !aligned(v, al) || !aligned(o, al) || !aligned(index, 4))
+    return SSBA_ERR_ARG;
+  const AttnArgs a = attn_args(d, s, q, k, v, index, o, dense);
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  hipError_t e = d->dtype == SSBA_DT_BF16 ? ssba::launch_attn_bf16(a, d->head_dim, d->tile, hs)
+                                          : ssba::launch_attn_f32(a, d->head_dim, d->tile, hs);
+  return e == hipSuccess ? SSBA_OK : SSBA_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ssba_abi_version(void) { return SSBA_ABI_VERSION; }
+
+const char* ssba_status_str(ssba_status s) {
+  switch (s) {
+    case SSBA_OK: return "ok";
+    case SSBA_ERR_ARG: return "invalid argument";
+    case SSBA_ERR_SHAPE: return "invalid shape";
+    case SSBA_ERR_UNSUPPORTED: return "unsupported configuration";
+    case SSBA_ERR_WORKSPACE: return "workspace too small";
+    case SSBA_ERR_NONFINITE: return "non-finite block affinity";
+    case SSBA_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+ssba_status ssba_workspace_size(const ssba_desc* d, size_t* index_bytes, size_t* scratch_bytes) {
+  Shape s;
+  const ssba_status st = check_desc(d, &s);
+  if (st != SSBA_OK) return st;
+  if (index_bytes) *index_bytes = index_bytes_of(d, s);
+  if (scratch_bytes) *scratch_bytes = scratch_bytes_of(d, s);
+  return SSBA_OK;
+}
+
+ssba_status ssba_build_index(const ssba_desc* d, const void* q, const void* k, int32_t* index,
+                             void* scratch, void* stream) {
+  Shape s;
+  const ssba_status st = check_desc(d, &s);
+  if (st != SSBA_OK) return st;
+  if (!index || !scratch || !aligned(index, 4) || !aligned(scratch, 8)) return SSBA_ERR_ARG;
+  const bool topk = d->gate == SSBA_GATE_TOPK;
+  if (topk) {
+    const size_t al = d->dtype == SSBA_DT_BF16 ? 2 : 4;
+    if (!q || !k || !aligned(q, al) || !aligned(k, al)) return SSBA_ERR_ARG;
+  }
+  IndexArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.q = q;
+  a.k = k;
+  a.index = index;
+  const size_t pooled = (size_t)d->batch * d->heads * s.n_tiles * d->head_dim;
+  double* base = static_cast<double*>(scratch);
+  a.qb = topk ? base : nullptr;
+  a.kb = topk ? base + pooled : nullptr;
+  a.flags = reinterpret_cast<int32_t*>(topk ? base + 2 * pooled : base);
+  a.sb = s.sb;
+  a.sh = s.sh;
+  a.st = s.st;
+  a.batch = d->batch;
+  a.heads = d->heads;
+  a.head_dim = d->head_dim;
+  a.n_tiles = s.n_tiles;
+  a.keep = d->keep;
+  a.win_h = d->win_h;
+  a.win_w = d->win_w;
+  a.ny = s.ny;
+  a.f = s.f;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  if (topk) {
+    e = ssba::launch_pool(a, d->dtype, hs);
+    if (e == hipSuccess) e = ssba::launch_gate_topk(a, hs);
+  } else {
+    e = ssba::launch_gate_static(a, d->gate, hs);
+  }
+  return e == hipSuccess ? SSBA_OK : SSBA_ERR_HIP;
+}
+
+ssba_status ssba_forward(const ssba_desc* d, const void* q, const void* k, const void* v,
+                         const int32_t* index, void* o, void* stream) {
+  return run_attention(d, q, k, v, index, o, stream, false);
+}
+
+ssba_status ssba_forward_dense(const ssba_desc* d, const void* q, const void* k, const void* v,
+                               void* o, void* stream) {
+  return run_attention(d, q, k, v, nullptr, o, stream, true);
+}
+
+ssba_status ssba_read_device_status(const ssba_desc* d, const void* scratch, ssba_status* out,
+                                    void* stream) {
+  Shape s;
+  const ssba_status st = check_desc(d, &s);
+  if (st != SSBA_OK) return st;
+  if (!scratch || !out || !aligned(scratch, 8)) return SSBA_ERR_ARG;
+  const size_t n = (size_t)d->batch * d->heads * s.n_tiles;
+  const size_t pooled = d->gate == SSBA_GATE_TOPK ? (size_t)16 * n * d->head_dim : 0;
+  const int32_t* flags = reinterpret_cast<const int32_t*>(static_cast<const char*>(scratch) + pooled);
+  std::vector<int32_t> host(n);
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (hipMemcpyAsync(host.data(), flags, n * sizeof(int32_t), hipMemcpyDeviceToHost, hs) != hipSuccess)
+    return SSBA_ERR_HIP;
+  if (hipStreamSynchronize(hs) != hipSuccess) return SSBA_ERR_HIP;
+  int32_t any = 0;
+  for (int32_t f : host) any |= f;
+  *out = any ? SSBA_ERR_NONFINITE : SSBA_OK;
+  return SSBA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,171 @@
+"""Torch-facing binding of the SSBA forward library (libssba.so).
+
+Thin marshalling layer over the C ABI in include/ssba.h: it checks tensors,
+fills the descriptor, allocates the index and scratch buffers with torch and
+passes raw device pointers plus the current HIP stream.  Every step of the
+computation runs in the HIP kernels; importing this module fails if the
+library is not built.
+
+Tensors are [B, H, T, D] (any strides with a unit channel stride, shared by
+Q, K, V and O), T = n_text + grid_h * grid_w, text rows first.
+"""
+from __future__ import annotations
+
+import math
+from typing import Optional, Tuple
+
+import torch
+
+from . import _lib
+
+_lib.load()   # fail loudly at import if the HIP library is missing
+
+__all__ = ["make_desc", "desc_for", "alloc_workspace", "build_index", "forward", "forward_dense",
+           "attention", "read_status", "layer_shift", "keep_from_rho", "SsbaError"]
+
+SsbaError = _lib.SsbaError
+_GATES = {"topk": _lib.GATE_TOPK, "window": _lib.GATE_WINDOW, "dense": _lib.GATE_DENSE}
+_DTYPES = {torch.bfloat16: _lib.DT_BF16, torch.float32: _lib.DT_F32}
+
+
+def layer_shift(layer: int, tile: int) -> Tuple[int, int]:
+    """Grid offset of DiT layer `layer`: (+tile/2, +tile/2) on even layers and
+    (-tile/2, -tile/2) on odd ones (Section 2.2.2; +-4 for 8x8 blocks)."""
+    h = tile // 2
+    return (h, h) if layer % 2 == 0 else (-h, -h)
+
+
+def keep_from_rho(n_tiles: int, rho: float) -> int:
+    """Key blocks kept per query block when floor(T_b * rho) are dropped
+    (Section 2.2.1, Top-k Gating)."""
+    return n_tiles - int(math.floor(float(n_tiles) * float(rho)))
+
+
+def make_desc(*, batch: int, heads: int, head_dim: int, grid: Tuple[int, int], tile: int,
+              shift: Tuple[int, int] = (0, 0), n_text: int = 0, gate: str = "topk", keep: int = 0,
+              window: Tuple[int, int] = (1, 1), dtype=torch.bfloat16, scale: Optional[float] = None,
+              strides: Optional[Tuple[int, int, int]] = None) -> _lib.SsbaDesc:
+    d = _lib.SsbaDesc()
+    d.batch, d.heads, d.head_dim = int(batch), int(heads), int(head_dim)
+    d.grid_h, d.grid_w, d.tile = int(grid[0]), int(grid[1]), int(tile)
+    d.shift_y, d.shift_x = int(shift[0]), int(shift[1])
+    d.n_text = int(n_text)
+    d.gate = _GATES[gate]
+    d.keep = int(keep)
+    d.win_h, d.win_w = int(window[0]), int(window[1])
+    d.dtype = _DTYPES[dtype]
+    d.softmax_scale = float(scale) if scale is not None else 0.0
+    sb, sh, st = strides if strides is not None else (0, 0, 0)
+    d.stride_b, d.stride_h, d.stride_t = int(sb), int(sh), int(st)
+    return d
+
+
+def desc_for(q: torch.Tensor, **kw) -> _lib.SsbaDesc:
+    """Descriptor for tensors shaped like `q` ([B, H, T, D])."""
+    if q.dim() != 4:
+        raise ValueError("expected a [B, H, T, D] tensor")
+    b, h, t, dd = q.shape
+    sb, sh, st, sc = q.stride()
+    if sc != 1:
+        raise ValueError("channel stride must be 1")
+    desc = make_desc(batch=b, heads=h, head_dim=dd, dtype=q.dtype, strides=(sb, sh, st), **kw)
+    if desc.n_text + desc.grid_h * desc.grid_w != t:
+        raise ValueError(f"sequence length {t} != n_text + grid_h * grid_w")
+    return desc
+
+
+def _check_tensors(desc, *ts):
+    ref = ts[0]
+    for t in ts:
+        if not isinstance(t, torch.Tensor) or not t.is_cuda:
+            raise ValueError("SSBA tensors must be GPU tensors")
+        if t.device != ref.device:
+            raise ValueError("all tensors must be on one device")
+        if t.dtype != ref.dtype or _DTYPES.get(t.dtype) != desc.dtype:
+            raise ValueError("Q, K, V and O must share the descriptor's dtype")
+        if t.shape != ref.shape or t.stride() != ref.stride():
+            raise ValueError("Q, K, V and O must share shape and strides")
+
+
+def _stream(dev) -> int:
+    return torch.cuda.current_stream(dev).cuda_stream
+
+
+def alloc_workspace(desc, device) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Index (int32 [B, H, T_b, 1 + T_b]) and scratch buffers for `desc`."""
+    ib, sb = _lib.workspace_size(desc)
+    tb = desc.grid_h * desc.grid_w // (desc.tile * desc.tile)
+    index = torch.empty((desc.batch, desc.heads, tb, tb + 1), dtype=torch.int32, device=device)
+    assert index.numel() * 4 == ib
+    scratch = torch.empty(((sb + 7) // 8,), dtype=torch.float64, device=device)
+    return index, scratch
+
+
+def build_index(q, k, desc, index=None, scratch=None):
+    """Gate (top-k / window / dense) -> index.  Returns (index, scratch)."""
+    if desc.gate == _lib.GATE_TOPK:
+        _check_tensors(desc, q, k)
+        dev = q.device
+    else:
+        dev = q.device if isinstance(q, torch.Tensor) else torch.device("cuda", torch.cuda.current_device())
+    if index is None or scratch is None:
+        index, scratch = alloc_workspace(desc, dev)
+    ib, sb = _lib.workspace_size(desc)
+    if not (index.is_cuda and scratch.is_cuda and index.dtype == torch.int32 and index.is_contiguous()
+            and index.numel() * 4 >= ib and scratch.numel() * scratch.element_size() >= sb):
+        raise ValueError("index / scratch buffers too small or not on the GPU")
+    qp = q.data_ptr() if desc.gate == _lib.GATE_TOPK else None
+    kp = k.data_ptr() if desc.gate == _lib.GATE_TOPK else None
+    _lib.check(_lib.build_index(desc, qp, kp, index.data_ptr(), scratch.data_ptr(), _stream(dev)),
+               "ssba_build_index")
+    return index, scratch
+
+
+def forward(q, k, v, index, desc, out=None):
+    """SSBA attention of every row (text rows included) into `out`."""
+    if out is None:
+        out = torch.empty_strided(q.shape, q.stride(), dtype=q.dtype, device=q.device)
+    _check_tensors(desc, q, k, v, out)
+    if not (index.is_cuda and index.dtype == torch.int32 and index.is_contiguous()):
+        raise ValueError("index must be a contiguous int32 GPU tensor")
+    ib, _ = _lib.workspace_size(desc)
+    if index.numel() * 4 < ib:
+        raise ValueError("index buffer too small")
+    _lib.check(_lib.forward(desc, q.data_ptr(), k.data_ptr(), v.data_ptr(), index.data_ptr(),
+                            out.data_ptr(), _stream(q.device)), "ssba_forward")
+    return out
+
+
+def forward_dense(q, k, v, desc, out=None):
+    """Dense attention over all T keys, same kernel family."""
+    if out is None:
+        out = torch.empty_strided(q.shape, q.stride(), dtype=q.dtype, device=q.device)
+    _check_tensors(desc, q, k, v, out)
+    _lib.check(_lib.forward_dense(desc, q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                  _stream(q.device)), "ssba_forward_dense")
+    return out
+
+
+def read_status(desc, scratch) -> int:
+    """Synchronize and return SSBA_OK or SSBA_ERR_NONFINITE from the last gate."""
+    return _lib.read_device_status(desc, scratch.data_ptr(), _stream(scratch.device))
+
+
+def attention(q, k, v, *, grid, tile, shift=None, layer=None, rho=None, keep=None, gate="topk",
+              window=None, n_text=0, scale=None, return_text=True):
+    """One SSBA layer call: gate, then attention.
+
+    `layer` selects the alternating +-tile/2 shift; `rho` is converted to the
+    kept-block count.  Returns O ([B, H, T, D]) or, with return_text=False,
+    only its image rows (Algorithm 1's return value).
+    """
+    if shift is None:
+        shift = layer_shift(layer, tile) if layer is not None else (0, 0)
+    tb = (grid[0] // tile) * (grid[1] // tile)
+    if gate == "topk" and keep is None:
+        keep = keep_from_rho(tb, 0.75 if rho is None else rho)
+    desc = desc_for(q, grid=grid, tile=tile, shift=shift, n_text=n_text, gate=gate,
+                    keep=keep or 0, window=window or (1, 1), scale=scale)
+    index, _ = build_index(q, k, desc)
+    o = forward(q, k, v, index, desc)
+    return o if return_text else o[:, :, n_text:]

@@ -1,0 +1,114 @@
+"""Host-side checks of the C ABI (no GPU needed, nothing is launched): the
+library loads, exports every function include/ssba.h declares, sizes its
+workspace as documented and rejects bad descriptors before any launch."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2605_15684_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ssba.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2605_15684_amd import build
+        build.build()
+    return _lib.load()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ssba_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared_functions()
+    assert set(names) == set(_lib.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_version_and_status_strings(lib):
+    assert lib.ssba_abi_version() == 1
+    seen = set()
+    for s in range(7):
+        txt = _lib.status_str(s)
+        assert txt and txt != "unknown status"
+        seen.add(txt)
+    assert len(seen) == 7
+    assert _lib.status_str(99) == "unknown status"
+
+
+def _desc(**kw):
+    d = _lib.SsbaDesc()
+    base = dict(batch=1, heads=16, head_dim=64, grid_h=64, grid_w=64, tile=8, shift_y=4, shift_x=4,
+                n_text=0, gate=_lib.GATE_TOPK, keep=10, win_h=1, win_w=1, dtype=_lib.DT_BF16,
+                softmax_scale=0.0, stride_b=0, stride_h=0, stride_t=0)
+    base.update(kw)
+    for k, v in base.items():
+        setattr(d, k, v)
+    return d
+
+
+@pytest.mark.parametrize("kw,index_bytes,scratch_bytes", [
+    ({}, 4 * 16 * 64 * 65, 16 * 16 * 64 * 64 + 4 * 16 * 64),
+    ({"gate": _lib.GATE_WINDOW, "win_h": 2, "win_w": 2}, 4 * 16 * 64 * 65, 4 * 16 * 64),
+    ({"gate": _lib.GATE_DENSE, "batch": 2, "heads": 24, "n_text": 256}, 4 * 48 * 64 * 65, 4 * 48 * 64),
+    ({"grid_h": 128, "grid_w": 128, "tile": 16, "head_dim": 128, "keep": 7},
+     4 * 16 * 64 * 65, 16 * 16 * 64 * 128 + 4 * 16 * 64),
+    ({"grid_h": 16, "grid_w": 16, "tile": 4, "heads": 2, "keep": 4, "dtype": _lib.DT_F32},
+     4 * 2 * 16 * 17, 16 * 2 * 16 * 64 + 4 * 2 * 16),
+])
+def test_workspace_sizes(lib, kw, index_bytes, scratch_bytes):
+    assert _lib.workspace_size(_desc(**kw)) == (index_bytes, scratch_bytes)
+
+
+@pytest.mark.parametrize("kw,status", [
+    ({"batch": 0}, _lib.SSBA_ERR_SHAPE),
+    ({"heads": -1}, _lib.SSBA_ERR_SHAPE),
+    ({"n_text": -3}, _lib.SSBA_ERR_SHAPE),
+    ({"grid_h": 60}, _lib.SSBA_ERR_SHAPE),
+    ({"head_dim": 96}, _lib.SSBA_ERR_UNSUPPORTED),
+    ({"tile": 32}, _lib.SSBA_ERR_UNSUPPORTED),
+    ({"grid_h": 512, "grid_w": 512}, _lib.SSBA_ERR_UNSUPPORTED),   # 4096 blocks > 1024
+    ({"dtype": 7}, _lib.SSBA_ERR_ARG),
+    ({"gate": 9}, _lib.SSBA_ERR_ARG),
+    ({"keep": 0}, _lib.SSBA_ERR_ARG),
+    ({"keep": 65}, _lib.SSBA_ERR_ARG),
+    ({"gate": _lib.GATE_WINDOW, "win_h": 3, "win_w": 1}, _lib.SSBA_ERR_ARG),
+    ({"gate": _lib.GATE_WINDOW, "win_h": 0, "win_w": 1}, _lib.SSBA_ERR_ARG),
+    ({"softmax_scale": float("nan")}, _lib.SSBA_ERR_ARG),
+    ({"stride_b": 1, "stride_h": 1, "stride_t": 32}, _lib.SSBA_ERR_SHAPE),
+    ({"stride_b": 64 * 4096 * 16, "stride_h": 64 * 4096, "stride_t": 68}, _lib.SSBA_ERR_UNSUPPORTED),
+])
+def test_bad_descriptors_rejected_before_launch(lib, kw, status):
+    d = _desc(**kw)
+    ib, sb = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    assert lib.ssba_workspace_size(ctypes.byref(d), ctypes.byref(ib), ctypes.byref(sb)) == status
+    # Every entry point validates the descriptor first; pointers are never touched.
+    assert _lib.build_index(d, None, None, None, None, None) == status
+    assert _lib.forward(d, None, None, None, None, None, None) == status
+    assert _lib.forward_dense(d, None, None, None, None, None) == status
+
+
+def test_null_pointers_rejected(lib):
+    d = _desc()
+    assert _lib.build_index(d, None, None, None, None, None) == _lib.SSBA_ERR_ARG
+    assert _lib.forward(d, None, None, None, None, None, None) == _lib.SSBA_ERR_ARG
+    assert _lib.forward_dense(d, None, None, None, None, None) == _lib.SSBA_ERR_ARG
+    assert lib.ssba_workspace_size(None, None, None) == _lib.SSBA_ERR_ARG
+    out = ctypes.c_int(0)
+    assert lib.ssba_read_device_status(ctypes.byref(d), None, ctypes.byref(out), None) == _lib.SSBA_ERR_ARG
+
+
+def test_misaligned_pointers_rejected(lib):
+    d = _desc()
+    # bf16 attention needs 16-byte aligned bases; rejected before any launch.
+    assert _lib.forward(d, 0x1002, 0x2000, 0x3000, 0x4000, 0x5000, None) == _lib.SSBA_ERR_ARG
+    assert _lib.build_index(d, 0x1000, 0x2000, 0x3002, 0x4000, None) == _lib.SSBA_ERR_ARG

@@ -1,0 +1,214 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle on
+the same seeded inputs.  Index lists must match bit for bit; outputs within
+2e-2 max-abs for bf16 inputs and 1e-5 for fp32."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import ssba_oracle as O
+from paper_2605_15684_amd.inputs import (PRESETS, SWEEP_TOPK_KEEP, SWEEP_WINDOW, Workload, make_qkv,
+                                         preset, workload_from)
+
+from _parity import (BF16_TOL, F32_TOL, gpu_desc, inputs, max_err, oracle_index, oracle_kw,
+                      run_gpu, sample_rows, to64, tol)
+
+pytestmark = pytest.mark.gpu
+
+
+# ---------------------------------------------------------------- index --
+INDEX_CASES = [
+    preset("tiny"), preset("tiny", shift=(-2, -2)),
+    preset("tiny", gate="window", window=(1, 1), shift=(0, 0)),
+    preset("tiny", gate="window", window=(1, 1), shift=(2, 2)),
+    preset("tiny", gate="window", window=(2, 4), shift=(1, -3)),
+    preset("tiny", gate="dense"), preset("tiny", keep=1), preset("tiny", keep=16),
+    preset("grid64"), preset("grid64", shift=(-4, -4)),
+    preset("grid64_text"), preset("grid128"),
+] + [preset("sweep64", keep=k) for k in SWEEP_TOPK_KEEP.values()] \
+  + [preset("sweep64", gate="window", window=w) for w in SWEEP_WINDOW.values()]
+
+
+@pytest.mark.parametrize("w", INDEX_CASES, ids=lambda w: f"{w.name}-{w.gate}-k{w.keep}-w{w.window}-s{w.shift}")
+def test_index_bit_exact(w):
+    (q, k, _), (qg, kg, _) = inputs(w)
+    from paper_2605_15684_amd import ssba
+    desc = gpu_desc(w, qg)
+    index, scratch = ssba.build_index(qg, kg, desc)
+    got = index.cpu().numpy()
+    want = oracle_index(w, q, k)
+    assert got.dtype == want.dtype == np.int32 and got.shape == want.shape
+    assert np.array_equal(got, want)
+    assert ssba.read_status(desc, scratch) == 0
+    if w.gate == "topk":
+        assert (got[..., 0] == w.keep).all()
+
+
+# ------------------------------------------------------- small, full output --
+SMALL = [
+    preset("tiny"),                                                  # fp32, 4x4 blocks
+    preset("tiny", shift=(-2, -2)),
+    preset("tiny", gate="window", window=(1, 1), shift=(0, 0)),
+    preset("tiny", gate="window", window=(1, 1), shift=(2, 2)),
+    preset("tiny", gate="dense"),
+    preset("tiny", n_text=7, heads=1),                               # fp32 ragged text
+    preset("tiny", head_dim=128, tile=8, keep=2, shift=(4, 4)),      # fp32 D128, 8x8
+    workload_from(batch=1, heads=2, grid_h=32, grid_w=32, head_dim=64, tile=8, keep=4, shift=(4, 4)),
+    workload_from(batch=2, heads=1, grid_h=32, grid_w=32, head_dim=64, tile=8, keep=5, shift=(-4, -4),
+                  n_text=77),                                        # ragged text tail
+    workload_from(batch=1, heads=2, grid_h=32, grid_w=16, head_dim=64, tile=8, keep=1, shift=(3, -5),
+                  n_text=64),
+    workload_from(batch=1, heads=2, grid_h=64, grid_w=64, head_dim=128, tile=16, keep=3, shift=(8, 8),
+                  heavy_key_rows=40),
+    workload_from(batch=1, heads=2, grid_h=32, grid_w=32, head_dim=128, tile=8, keep=6, shift=(4, 4),
+                  n_text=13),
+    workload_from(batch=1, heads=2, grid_h=64, grid_w=32, head_dim=64, tile=16, keep=2, shift=(-8, 8)),
+    workload_from(batch=1, heads=2, grid_h=16, grid_w=16, head_dim=64, tile=4, keep=5, shift=(2, 2)),
+    workload_from(batch=1, heads=1, grid_h=16, grid_w=32, head_dim=128, tile=4, keep=7, shift=(1, 2),
+                  n_text=20),
+    workload_from(batch=1, heads=2, grid_h=32, grid_w=32, head_dim=64, tile=8, gate="window",
+                  window=(2, 2), shift=(4, 4)),
+    workload_from(batch=1, heads=2, grid_h=32, grid_w=32, head_dim=64, tile=8, gate="dense", n_text=5),
+]
+
+
+def _ids(w: Workload):
+    return f"{w.name}-{w.dtype}-D{w.head_dim}-B{w.tile}-{w.gate}{w.keep}-t{w.n_text}-s{w.shift}"
+
+
+@pytest.mark.parametrize("w", SMALL, ids=_ids)
+def test_output_small_full(w):
+    (q, k, v), (qg, kg, vg) = inputs(w)
+    index, out = run_gpu(w, qg, kg, vg)
+    want_idx = oracle_index(w, q, k)
+    assert np.array_equal(index, want_idx)
+    ref = O.attention(to64(q), to64(k), to64(v), want_idx, **oracle_kw(w))
+    got = out.float().cpu().double().numpy()
+    err = np.abs(got - ref).max()
+    assert np.isfinite(got).all()
+    assert err <= tol(w), f"max-abs {err:.3e}"
+
+
+@pytest.mark.parametrize("w", [preset("tiny"), preset("tiny", n_text=9, heads=1),
+                               workload_from(batch=1, heads=2, grid_h=32, grid_w=32, head_dim=64,
+                                             tile=8, n_text=70),
+                               workload_from(batch=1, heads=1, grid_h=32, grid_w=32, head_dim=128,
+                                             tile=16, n_text=3)], ids=_ids)
+def test_dense_path_small(w):
+    (q, k, v), (qg, kg, vg) = inputs(w)
+    _, out = run_gpu(w, qg, kg, vg, dense=True)
+    idx = O.build_index(to64(q), to64(k), gate="dense", **oracle_kw(w))
+    ref = O.attention(to64(q), to64(k), to64(v), idx, **oracle_kw(w))
+    err = np.abs(out.float().cpu().double().numpy() - ref).max()
+    assert err <= tol(w), f"max-abs {err:.3e}"
+
+
+# -------------------------------------------- full size, sampled outputs --
+FULL = [preset("grid64"), preset("grid64", shift=(-4, -4)), preset("grid64_text"), preset("grid128"),
+        preset("sweep64")]
+
+
+@pytest.mark.parametrize("w", FULL, ids=_ids)
+def test_output_full_size_sampled(w):
+    (q, k, v), (qg, kg, vg) = inputs(w)
+    index, out = run_gpu(w, qg, kg, vg)
+    want_idx = oracle_index(w, q, k)
+    assert np.array_equal(index, want_idx)
+    rng = np.random.default_rng(123)
+    heads = [(0, 0), (w.batch - 1, w.heads - 1), (int(rng.integers(w.batch)), int(rng.integers(w.heads)))]
+    rows = sample_rows(w, rng)
+    ref = O.attention(to64(q), to64(k), to64(v), want_idx, rows=rows, heads=heads, **oracle_kw(w))
+    err = max_err(out, ref, heads, rows)
+    assert err <= BF16_TOL, f"max-abs {err:.3e}"
+
+
+@pytest.mark.parametrize("w", [preset("grid64"), preset("grid64_text")], ids=_ids)
+def test_dense_path_full_size_sampled(w):
+    (q, k, v), (qg, kg, vg) = inputs(w)
+    _, out = run_gpu(w, qg, kg, vg, dense=True)
+    rng = np.random.default_rng(7)
+    heads = [(0, 0), (w.batch - 1, w.heads - 1)]
+    rows = sample_rows(w, rng)
+    idx = O.build_index(to64(q[:1, :1]), to64(k[:1, :1]), gate="dense", **oracle_kw(w))
+    idx = np.broadcast_to(idx, (w.batch, w.heads) + idx.shape[2:])
+    ref = O.attention(to64(q), to64(k), to64(v), idx, rows=rows, heads=heads, **oracle_kw(w))
+    assert max_err(out, ref, heads, rows) <= BF16_TOL
+
+
+# -------------------------------------------------------------- properties --
+def test_rows_sum_to_one_via_ones_values():
+    w = preset("grid64_text", batch=1, heads=2)
+    (q, k, _), (qg, kg, _) = inputs(w)
+    vg = torch.ones_like(qg)
+    _, out = run_gpu(w, qg, kg, vg)
+    assert (out.float() - 1.0).abs().max().item() <= BF16_TOL / 4
+
+
+def test_deterministic_and_stride_independent():
+    w = preset("grid64_text", batch=1, heads=4)
+    (_, _, _), (qg, kg, vg) = inputs(w)
+    i1, o1 = run_gpu(w, qg, kg, vg)
+    i2, o2 = run_gpu(w, qg, kg, vg)
+    assert np.array_equal(i1, i2) and torch.equal(o1, o2)
+    # Same data stored as [B, T, H, D] and viewed as [B, H, T, D].
+    qs, ks, vs = (t.transpose(1, 2).contiguous().transpose(1, 2) for t in (qg, kg, vg))
+    assert qs.stride() != qg.stride()
+    i3, o3 = run_gpu(w, qs, ks, vs)
+    assert np.array_equal(i1, i3) and torch.equal(o1, o3.contiguous())
+
+
+def test_nonfinite_input_sets_status():
+    from paper_2605_15684_amd import ssba
+    w = preset("grid64", heads=2)
+    (_, _, _), (qg, kg, _) = inputs(w)
+    desc = gpu_desc(w, qg)
+    _, scratch = ssba.build_index(qg, kg, desc)
+    assert ssba.read_status(desc, scratch) == 0
+    kg2 = kg.clone()
+    kg2[0, 1, 100, 5] = float("nan")
+    _, scratch = ssba.build_index(qg, kg2, desc)
+    assert ssba.read_status(desc, scratch) == 5
+
+
+def test_permutation_within_a_block():
+    w = preset("grid64", heads=2)
+    (q, k, v), (qg, kg, vg) = inputs(w)
+    tiles = O.frame_tiles(w.grid_h, w.grid_w, w.tile, *w.shift)
+    rng = np.random.default_rng(0)
+    perm = np.arange(w.t_img)
+    for t in range(tiles.shape[0]):
+        perm[tiles[t]] = tiles[t][rng.permutation(tiles.shape[1])]
+    p = torch.tensor(perm, device="cuda")
+    i1, o1 = run_gpu(w, qg, kg, vg)
+    i2, o2 = run_gpu(w, qg, kg[:, :, p], vg[:, :, p])
+    assert np.array_equal(i1, i2)
+    assert (o1.float() - o2.float()).abs().max().item() <= BF16_TOL
+    i3, o3 = run_gpu(w, qg[:, :, p], kg, vg)
+    assert np.array_equal(i1, i3)
+    assert (o3.float() - o1[:, :, p].float()).abs().max().item() <= BF16_TOL
+
+
+def test_half_block_offsets_agree():
+    w = preset("grid64", heads=2)
+    (_, _, _), (qg, kg, vg) = inputs(w)
+    _, a = run_gpu(w.with_(shift=(4, 4)), qg, kg, vg)
+    _, b = run_gpu(w.with_(shift=(-4, -4)), qg, kg, vg)
+    assert (a.float() - b.float()).abs().max().item() <= BF16_TOL
+
+
+def test_zero_sparsity_equals_dense_path():
+    w = preset("grid64", heads=2, keep=64)
+    (_, _, _), (qg, kg, vg) = inputs(w)
+    _, a = run_gpu(w, qg, kg, vg)
+    _, b = run_gpu(w, qg, kg, vg, dense=True)
+    assert (a.float() - b.float()).abs().max().item() <= BF16_TOL
+
+
+def test_attention_convenience_call():
+    from paper_2605_15684_amd import ssba
+    w = preset("grid64_text", batch=1, heads=2)
+    (q, k, v), (qg, kg, vg) = inputs(w)
+    img = ssba.attention(qg, kg, vg, grid=(64, 64), tile=8, layer=0, keep=10, n_text=256,
+                         return_text=False)
+    assert img.shape == (1, 2, 4096, 64)
+    _, full = run_gpu(w, qg, kg, vg)
+    assert torch.equal(img, full[:, :, 256:])
