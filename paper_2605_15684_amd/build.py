@@ -24,6 +24,9 @@ SOURCES = {
     "ssba_index.hip": ["-ffp-contract=off"],
     "ssba_attn_bf16.hip": [],
     "ssba_attn_f32.hip": [],
+    # MFMA results in ordinary VGPRs: the softmax reads every score and the
+    # default accumulation-register form costs a copy per element.
+    "ssba_attn_w64.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
 }
 
 COMMON = [
