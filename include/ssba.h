@@ -28,6 +28,8 @@
  * row n_text + y * grid_w + x holds grid token (y, x).  Q, K, V and O share one
  * element-stride triple (stride_b, stride_h, stride_t); the channel stride is 1.
  * Passing all three strides as 0 selects the contiguous [B, H, T, D] layout.
+ * bf16 tensors must be 16-byte aligned with strides that are multiples of 8
+ * elements (16-byte row loads); f32 tensors 4-byte aligned.
  *
  * Shifted frame: with (sy, sx) reduced mod (grid_h, grid_w), block t =
  * (ty, tx) (row-major over the n_y x n_x block grid) and slot s (row-major
@@ -102,7 +104,7 @@ ssba_status ssba_workspace_size(const ssba_desc* d, size_t* index_bytes, size_t*
  * [B][H][T_b][1 + T_b]: entry 0 = count of kept key blocks, then their block
  * ids ascending, then -1 padding.  TOPK reads the image rows of q and k (dtype
  * d->dtype, layout above); WINDOW and DENSE read neither (q, k may be NULL).
- * `scratch` (scratch_bytes, any alignment >= 8) is overwritten; its status
+ * `scratch` (scratch_bytes, 16-byte aligned) is overwritten; its status
  * flags are read by ssba_read_device_status. */
 ssba_status ssba_build_index(const ssba_desc* d, const void* q, const void* k,
                              int32_t* index, void* scratch, void* hip_stream);

@@ -50,14 +50,23 @@ class SsbaError(RuntimeError):
 _lib = None
 
 
-def load(path: str = LIB_PATH) -> ctypes.CDLL:
-    """Load libssba.so once.  Raises ImportError if it is missing."""
+def load(path: str = None) -> ctypes.CDLL:
+    """Load libssba.so (or `path`) once.  Raises ImportError if it is missing."""
     global _lib
     if _lib is not None:
         return _lib
+    path = path or LIB_PATH
     if not os.path.exists(path):
         raise ImportError(f"{path} is not built; run `python -m paper_2605_15684_amd.build` "
                           "(the SSBA path has no CPU fallback)")
+    # PyTorch ships its own HIP runtime under the same soname.  Importing it
+    # first makes this library bind to that runtime, so kernels launched here
+    # run on torch's streams and memory; loaded the other way round the
+    # process would hold two runtimes.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(path)
     vp, sz = ctypes.c_void_p, ctypes.c_size_t
     dp = ctypes.POINTER(SsbaDesc)

@@ -177,10 +177,10 @@ ssba_status ssba_build_index(const ssba_desc* d, const void* q, const void* k, i
   Shape s;
   const ssba_status st = check_desc(d, &s);
   if (st != SSBA_OK) return st;
-  if (!index || !scratch || !aligned(index, 4) || !aligned(scratch, 8)) return SSBA_ERR_ARG;
+  if (!index || !scratch || !aligned(index, 4) || !aligned(scratch, 16)) return SSBA_ERR_ARG;
   const bool topk = d->gate == SSBA_GATE_TOPK;
   if (topk) {
-    const size_t al = d->dtype == SSBA_DT_BF16 ? 2 : 4;
+    const size_t al = d->dtype == SSBA_DT_BF16 ? 16 : 4;
     if (!q || !k || !aligned(q, al) || !aligned(k, al)) return SSBA_ERR_ARG;
   }
   IndexArgs a;

@@ -386,7 +386,7 @@ hipError_t launch_t(const AttnArgs& a0, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, int tile, hipStream_t s) {
-  if (w64_supported(head_dim, tile, a.dense != 0, a.n_tiles, (int64_t)a.seq * a.st))
+  if (w64_supported(head_dim, tile, a.dense != 0, a.n_tiles, a.seq, (int64_t)a.seq * a.st))
     return launch_attn_w64(a, s);
   if (head_dim == 64) {
     if (tile == 4) return launch_t<64, 2>(a, s);

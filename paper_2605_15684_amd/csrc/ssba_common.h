@@ -69,7 +69,7 @@ hipError_t launch_gate_static(const IndexArgs& a, int gate, hipStream_t s);
 hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, int tile, hipStream_t s);
 hipError_t launch_attn_f32(const AttnArgs& a, int head_dim, int tile, hipStream_t s);
 // One-wave-per-64-rows bf16 kernel for head_dim 64 (8x8 blocks or dense).
-bool w64_supported(int head_dim, int tile, bool dense, int n_tiles, int64_t span);
+bool w64_supported(int head_dim, int tile, bool dense, int n_tiles, int seq, int64_t span);
 hipError_t launch_attn_w64(const AttnArgs& a, hipStream_t s);
 
 }  // namespace ssba

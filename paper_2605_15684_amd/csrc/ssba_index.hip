@@ -9,6 +9,7 @@
 // -ffp-contract=off and the arithmetic is written with explicit
 // round-to-nearest intrinsics, so no multiply-add is ever fused.
 #include <hip/hip_runtime.h>
+#include <type_traits>
 #include <hip/hip_bf16.h>
 
 #include "ssba_common.h"
@@ -16,79 +17,129 @@
 namespace ssba {
 namespace {
 
-__device__ __forceinline__ double load_as_f64(const void* base, int64_t off, int dtype) {
-  if (dtype == SSBA_DT_F32) return (double)static_cast<const float*>(base)[off];
-  const uint16_t bits = static_cast<const uint16_t*>(base)[off];
-  return (double)__uint_as_float((uint32_t)bits << 16);  // bf16 -> f32 is exact
-}
-
-// One workgroup per (block t, head h, batch b); threads [0, D) pool Q channel
-// c, threads [D, 2D) pool K channel c.  Reads every image row of Q and K once.
-template <int DTYPE>
+// Block pooling.  One workgroup pools Q and K of one block.  The block's rows
+// are staged in LDS, up to 64 slots at a time, by all 256 threads with wide
+// loads; then 2 * D threads (one per channel of Q and of K) add the staged
+// slots in slot order in fp64, the ordered sum that makes the lists exact.
+// Pooled q is stored block-major [B][H][T_b][D]; pooled k channel-major
+// [B][H][D][T_b], so that the gate reads one channel of all key blocks with
+// one coalesced load.
+template <int DTYPE, int TILE_LOG2, int D>
 __global__ void __launch_bounds__(256) k_pool(IndexArgs a) {
+  constexpr int SLOTS = 1 << (2 * TILE_LOG2);
+  constexpr int SB = SLOTS < 64 ? SLOTS : 64;          // slots per stage
+  constexpr bool BF16 = DTYPE == SSBA_DT_BF16;
+  constexpr int EPV = BF16 ? 8 : 1;                    // elements per load
+  constexpr int VPR = D / EPV;                         // loads per token row
+  constexpr int LOADS = 2 * SB * VPR;                  // per stage, Q then K
+  using Vec = typename std::conditional<BF16, uint4, float>::type;
+  __shared__ Vec stage[LOADS];
   const int t = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int D = a.head_dim;
-  const int which = threadIdx.x / D;  // 0 = Q, 1 = K
-  const int c = threadIdx.x - which * D;
-  if (which > 1) return;
-  const void* src = which == 0 ? a.q : a.k;
-  double* dst = which == 0 ? a.qb : a.kb;
-  const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh + c;
-  const int slots = 1 << (2 * a.f.tile_log2);
-  double sum = load_as_f64(src, base + (int64_t)frame_row(a.f, t, 0) * a.st, DTYPE);
-  for (int s = 1; s < slots; ++s)
-    sum = __dadd_rn(sum, load_as_f64(src, base + (int64_t)frame_row(a.f, t, s) * a.st, DTYPE));
-  dst[(((int64_t)b * a.heads + h) * a.n_tiles + t) * D + c] = sum;
+  const int tid = threadIdx.x;
+  const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
+  const int which = tid / D, c = tid % D;              // summing threads: tid < 2D
+  double sum = 0.0;
+#pragma unroll 1
+  for (int s0 = 0; s0 < SLOTS; s0 += SB) {
+    static_assert(LOADS % 256 == 0, "whole rounds of loads");
+    Vec v[LOADS / 256];
+#pragma unroll
+    for (int r = 0; r < LOADS / 256; ++r) {
+      const int idx = tid + 256 * r;
+      const int tensor = idx / (SB * VPR), rem = idx % (SB * VPR);
+      const int slot = rem / VPR, part = rem % VPR;
+      const int64_t off = base + (int64_t)frame_row(a.f, t, s0 + slot) * a.st + part * EPV;
+      const void* src = tensor == 0 ? a.q : a.k;
+      v[r] = *reinterpret_cast<const Vec*>(static_cast<const char*>(src) + off * (BF16 ? 2 : 4));
+    }
+#pragma unroll
+    for (int r = 0; r < LOADS / 256; ++r) stage[tid + 256 * r] = v[r];
+    __syncthreads();
+    if (tid < 2 * D) {
+      const char* col = reinterpret_cast<const char*>(stage) +
+                        ((size_t)which * SB * D + c) * (BF16 ? 2 : 4);
+#pragma unroll 8
+      for (int u = 0; u < SB; ++u) {
+        double x;
+        if (BF16)   // bf16 -> f32 -> f64 is exact
+          x = (double)__uint_as_float((uint32_t)*reinterpret_cast<const uint16_t*>(col + (size_t)u * D * 2) << 16);
+        else
+          x = (double)*reinterpret_cast<const float*>(col + (size_t)u * D * 4);
+        sum = (s0 + u == 0) ? x : __dadd_rn(sum, x);
+      }
+    }
+    __syncthreads();
+  }
+  if (tid < 2 * D) {
+    const int64_t bh = (int64_t)b * a.heads + h;
+    if (which == 0)
+      a.qb[(bh * a.n_tiles + t) * D + c] = sum;
+    else
+      a.kb[(bh * D + c) * a.n_tiles + t] = sum;
+  }
 }
 
-// Strict total order used for ranking: a larger affinity first, NaN after every
-// number, equal values (including +0 / -0) by ascending block index.
-__device__ __forceinline__ bool ranks_before(double sa, int ja, double sb, int jb) {
-  const bool na = sa != sa, nb = sb != sb;
-  if (na || nb) return (!na) || (na && nb && ja < jb);
-  return sa > sb || (sa == sb && ja < jb);
+// Ranking key: an unsigned integer whose order is the gate's order on
+// affinities.  -0 is folded onto +0 and every NaN onto key 0, below all
+// numbers; equal keys are then ordered by ascending block index.
+__device__ __forceinline__ uint64_t rank_key(double s) {
+  if (s != s) return 0;
+  if (s == 0.0) s = 0.0;
+  const uint64_t u = (uint64_t)__double_as_longlong(s);
+  return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
 }
 
-// One workgroup per query block (i, h, b); thread j computes S[i][j] and its
-// rank.  Blocks ranked below `keep` are kept; the kept ids are written in
-// ascending order.
+// One workgroup per query block (i, h, b); thread j computes S[i][j] (the
+// channel-ordered sum of rounded products) and its rank.  The `keep` blocks of
+// lowest rank are kept and written in ascending block order.
 __global__ void __launch_bounds__(1024) k_gate_topk(IndexArgs a) {
-  extern __shared__ double smem[];
-  double* qrow = smem;                 // [D]
-  double* srow = smem + a.head_dim;    // [T_b]
-  __shared__ int keptf[1024];
+  extern __shared__ uint64_t keys[];   // [T_b]
+  __shared__ int wave_kept[16];
   __shared__ int bad;
   const int i = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int D = a.head_dim, tb = a.n_tiles;
-  const int j = threadIdx.x;
+  const int j = threadIdx.x, lane = j & 63, wave = j >> 6;
   const int64_t bh = (int64_t)b * a.heads + h;
   if (j == 0) bad = 0;
-  for (int c = j; c < D; c += blockDim.x) qrow[c] = a.qb[(bh * tb + i) * D + c];
   __syncthreads();
-  double s = 0.0;
+  uint64_t key = 0;
   if (j < tb) {
-    const double* kr = a.kb + (bh * tb + j) * D;
-    s = __dmul_rn(qrow[0], kr[0]);
-    for (int c = 1; c < D; ++c) s = __dadd_rn(s, __dmul_rn(qrow[c], kr[c]));
-    srow[j] = s;
+    const double* qr = a.qb + (bh * tb + i) * D;   // the same row for every thread
+    const double* kc = a.kb + bh * D * tb + j;     // channel c of block j at kc[c * tb]
+    double s = 0.0;
+    for (int c0 = 0; c0 < D; c0 += 32) {
+      double kv[32];
+#pragma unroll
+      for (int u = 0; u < 32; ++u) kv[u] = kc[(int64_t)(c0 + u) * tb];
+#pragma unroll
+      for (int u = 0; u < 32; ++u) {
+        const double p = __dmul_rn(qr[c0 + u], kv[u]);
+        s = (c0 + u == 0) ? p : __dadd_rn(s, p);
+      }
+    }
     if (!isfinite(s)) atomicOr(&bad, 1);
+    key = rank_key(s);
+    keys[j] = key;
   }
   __syncthreads();
-  int kept = 0;
+  bool kept = false;
   if (j < tb) {
     int rank = 0;
-    for (int jj = 0; jj < tb; ++jj) rank += ranks_before(srow[jj], jj, s, j) ? 1 : 0;
+    for (int jj = 0; jj < tb; ++jj) {
+      const uint64_t kj = keys[jj];
+      rank += (kj > key || (kj == key && jj < j)) ? 1 : 0;
+    }
     kept = rank < a.keep;
-    keptf[j] = kept;
   }
+  // Position of a kept block in the ascending list: kept blocks of lower id.
+  const uint64_t mask = __ballot(kept);
+  if (lane == 0) wave_kept[wave] = __popcll(mask);
   __syncthreads();
+  int pos = __popcll(mask & ((1ull << lane) - 1ull));
+  for (int w = 0; w < wave; ++w) pos += wave_kept[w];
   int32_t* out = a.index + (bh * tb + i) * (tb + 1);
   if (j < tb) {
-    if (kept) {
-      int pos = 0;
-      for (int jj = 0; jj < j; ++jj) pos += keptf[jj];
-      out[1 + pos] = j;
-    }
+    if (kept) out[1 + pos] = j;
     if (j >= a.keep) out[1 + j] = -1;
   }
   if (j == 0) {
@@ -127,20 +178,35 @@ __global__ void __launch_bounds__(1024) k_gate_static(IndexArgs a, int gate) {
 
 int round_threads(int n) { return ((n + 63) / 64) * 64; }
 
+template <int DTYPE, int D>
+void launch_pool_d(const IndexArgs& a, hipStream_t s) {
+  dim3 grid(a.n_tiles, a.heads, a.batch), block(256);
+  switch (a.f.tile_log2) {
+    case 2: hipLaunchKernelGGL((k_pool<DTYPE, 2, D>), grid, block, 0, s, a); break;
+    case 3: hipLaunchKernelGGL((k_pool<DTYPE, 3, D>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((k_pool<DTYPE, 4, D>), grid, block, 0, s, a); break;
+  }
+}
+
+template <int DTYPE>
+void launch_pool_t(const IndexArgs& a, hipStream_t s) {
+  if (a.head_dim == 64) launch_pool_d<DTYPE, 64>(a, s);
+  else launch_pool_d<DTYPE, 128>(a, s);
+}
+
 }  // namespace
 
 hipError_t launch_pool(const IndexArgs& a, int dtype, hipStream_t s) {
-  dim3 grid(a.n_tiles, a.heads, a.batch), block(2 * a.head_dim);
   if (dtype == SSBA_DT_F32)
-    hipLaunchKernelGGL(k_pool<SSBA_DT_F32>, grid, block, 0, s, a);
+    launch_pool_t<SSBA_DT_F32>(a, s);
   else
-    hipLaunchKernelGGL(k_pool<SSBA_DT_BF16>, grid, block, 0, s, a);
+    launch_pool_t<SSBA_DT_BF16>(a, s);
   return hipGetLastError();
 }
 
 hipError_t launch_gate_topk(const IndexArgs& a, hipStream_t s) {
   dim3 grid(a.n_tiles, a.heads, a.batch), block(round_threads(a.n_tiles));
-  size_t lds = sizeof(double) * (size_t)(a.head_dim + a.n_tiles);
+  size_t lds = sizeof(uint64_t) * (size_t)a.n_tiles;
   hipLaunchKernelGGL(k_gate_topk, grid, block, lds, s, a);
   return hipGetLastError();
 }
