@@ -1,7 +1,7 @@
 """Benchmark of the SSBA forward path on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload grid64]
-                    [--no-cpu] [--sweep]
+                    [--no-cpu] [--sweep] [--copy-calibration]
 
 One step = one SSBA layer call on inputs already resident in HBM: the top-k
 gate (block pooling, affinity, ranking -> index) followed by the block-sparse
@@ -11,6 +11,16 @@ per-configuration lines on stderr (sparsity sweep, text tokens, 2K grid).
 Flops are counted over computed (kept) query/key pairs only: 4 * D per pair
 (2 * D for Q K^T, 2 * D for P V).  Pairs per (batch, head):
 T_img * (keep * Bt^2 + T_txt) + T_txt * T.
+
+The roofline object describes the attention kernel (the dominant one): its
+flops per launch over its average launch time (HIP events on the stream it
+runs on).  `traffic` is the HBM traffic per launch measured with rocprofv3
+counters (FETCH_SIZE and WRITE_SIZE, scaled by what the same counters read
+for a plain copy of known size), reported only while the kernel's sources
+still hash to the values the counters were taken on.
+
+--copy-calibration runs only that plain copy (256 MiB, 5 times) for the
+counter runs and prints its size.
 """
 from __future__ import annotations
 
@@ -29,6 +39,38 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
+COPY_BYTES = 256 << 20
+
+# HBM traffic per launch from counter runs: kernel -> sources it was built
+# from (sha256 over their bytes, in order), FETCH_SIZE and WRITE_SIZE in KiB
+# per dispatch, and the copy calibration factors (bytes known / bytes read by
+# the counter).  Filled from the counter summaries kept with the profiles.
+MEASURED_TRAFFIC = {}
+
+
+def kernel_sources(kernel: str):
+    base = os.path.join(ROOT, "paper_2605_15684_amd", "csrc")
+    own = {"k_attn_w64": "ssba_attn_w64.hip", "k_attn_bf16": "ssba_attn_bf16.hip",
+           "k_attn_f32": "ssba_attn_f32.hip"}[kernel.split("<")[0]]
+    return [os.path.join(base, own), os.path.join(base, "ssba_common.h"),
+            os.path.join(ROOT, "include", "ssba.h")]
+
+
+def sources_sha(kernel: str) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in kernel_sources(kernel):
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str):
+    """HBM bytes per launch, or None if not measured on these sources."""
+    m = MEASURED_TRAFFIC.get(kernel)
+    if not m or m["sha"] != sources_sha(kernel):
+        return None
+    return m["fetch_kib"] * 1024 * m["fetch_factor"] + m["write_kib"] * 1024 * m["write_factor"]
 
 
 def pairs_per_bh(w, keep=None) -> int:
@@ -174,6 +216,7 @@ def main():
     ap.add_argument("--workload", default="grid64")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--sweep", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the SSBA path has no multi-GPU mode in this build "
@@ -183,14 +226,26 @@ def main():
     import torch
     from paper_2605_15684_amd.inputs import SWEEP_TOPK_KEEP, SWEEP_WINDOW, preset
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.copy_calibration:
+        src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": COPY_BYTES, "calls": 5}), flush=True)
+        return
 
     w = preset(args.workload)
     r, m = measure(w, args.steps, args.warmup, max(20, args.steps // 4))
     f = flops(w)
     achieved = f / (m["ms_fwd"] * 1e-3) / 1e12
-    roofline = {"bound": "mfma", "kernel": "k_attn_bf16", "achieved": round(achieved, 2),
+    from paper_2605_15684_amd import _lib
+    kernel = _lib.forward_kernel(r.desc)
+    traffic = measured_traffic(kernel)
+    roofline = {"bound": "mfma", "kernel": kernel, "achieved": round(achieved, 2),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": None}
+                "traffic": None if traffic is None else round(traffic),
+                "traffic_unit": "HBM bytes/launch", "sources_sha": sources_sha(kernel)}
     cpu = None if args.no_cpu else cpu_baseline(r)
     line = {
         "metric": "SSBA fwd ms/call + effective TFLOP/s (% bf16 MFMA peak) at 4096 tokens, 84% sparse",

@@ -127,6 +127,12 @@ ssba_status ssba_forward(const ssba_desc* d, const void* q, const void* k, const
 ssba_status ssba_forward_dense(const ssba_desc* d, const void* q, const void* k, const void* v,
                                void* o, void* hip_stream);
 
+/* Name of the attention kernel that ssba_forward (dense = 0) or
+ * ssba_forward_dense (dense != 0) launches for this descriptor, as profilers
+ * show it without namespace and arguments (e.g. "k_attn_w64<false>"); NULL if
+ * the descriptor is invalid.  Static storage; launches nothing. */
+const char* ssba_forward_kernel(const ssba_desc* d, int dense);
+
 /* Synchronizes `hip_stream`, then reads the status flags that the last
  * ssba_build_index left in `scratch` (same descriptor): SSBA_OK, or
  * SSBA_ERR_NONFINITE if any affinity row held a NaN or Inf (TOPK only). */

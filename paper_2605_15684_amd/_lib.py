@@ -26,7 +26,8 @@ GATE_WINDOW = 1
 GATE_DENSE = 2
 
 EXPORTS = ("ssba_abi_version", "ssba_status_str", "ssba_workspace_size", "ssba_build_index",
-           "ssba_forward", "ssba_forward_dense", "ssba_read_device_status")
+           "ssba_forward", "ssba_forward_dense", "ssba_read_device_status",
+           "ssba_forward_kernel")
 
 
 class SsbaDesc(ctypes.Structure):
@@ -82,6 +83,8 @@ def load(path: str = None) -> ctypes.CDLL:
     lib.ssba_forward.argtypes = [dp, vp, vp, vp, vp, vp, vp]
     lib.ssba_forward_dense.restype = ctypes.c_int
     lib.ssba_forward_dense.argtypes = [dp, vp, vp, vp, vp, vp]
+    lib.ssba_forward_kernel.restype = ctypes.c_char_p
+    lib.ssba_forward_kernel.argtypes = [dp, ctypes.c_int]
     lib.ssba_read_device_status.restype = ctypes.c_int
     lib.ssba_read_device_status.argtypes = [dp, vp, ctypes.POINTER(ctypes.c_int), vp]
     _lib = lib
@@ -121,3 +124,9 @@ def read_device_status(desc, scratch_ptr, stream):
     check(load().ssba_read_device_status(ctypes.byref(desc), scratch_ptr, ctypes.byref(out), stream),
           "ssba_read_device_status")
     return out.value
+
+
+def forward_kernel(desc, dense: bool = False):
+    """Name of the kernel ssba_forward (or ssba_forward_dense) would launch."""
+    name = load().ssba_forward_kernel(ctypes.byref(desc), 1 if dense else 0)
+    return None if name is None else name.decode()

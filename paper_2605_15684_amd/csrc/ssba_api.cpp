@@ -216,6 +216,13 @@ ssba_status ssba_build_index(const ssba_desc* d, const void* q, const void* k, i
   return e == hipSuccess ? SSBA_OK : SSBA_ERR_HIP;
 }
 
+const char* ssba_forward_kernel(const ssba_desc* d, int dense) {
+  Shape s;
+  if (check_desc(d, &s, !dense) != SSBA_OK) return nullptr;
+  const AttnArgs a = attn_args(d, s, nullptr, nullptr, nullptr, nullptr, nullptr, dense != 0);
+  return ssba::attn_kernel_name(a, d->head_dim, d->tile, d->dtype);
+}
+
 ssba_status ssba_forward(const ssba_desc* d, const void* q, const void* k, const void* v,
                          const int32_t* index, void* o, void* stream) {
   return run_attention(d, q, k, v, index, o, stream, false);

@@ -5,17 +5,25 @@
 // dense control).  Computes the attend step of Algorithm 1 like the generic
 // kernel; it differs only in how data reaches the matrix cores.
 //
-// At head_dim 64 a 64x64 block pair costs about the same in MFMA cycles,
-// softmax VALU cycles and bytes moved, so:
+// At head_dim 64 the softmax of a 64x64 block pair costs as many VALU cycles
+// as its two products cost MFMA cycles, so the kernel is built to overlap
+// them:
 //   * a workgroup owns the 64 query rows of one block; its two waves take 32
-//     rows each, so even one workgroup per SIMD pair keeps two waves resident
-//     per SIMD to overlap one wave's softmax with the other's MFMAs;
+//     rows each;
 //   * every 64-key chunk of K and V is copied once per workgroup, by DMA
-//     (global_load_lds_dwordx4; each wave moves half of it), into
-//     double-buffered LDS, so each byte of K/V is fetched once per query block;
+//     (buffer_load_dwordx4 ... lds; each wave moves half of it), into
+//     double-buffered LDS.  Row offsets are scalar operands and the per-lane
+//     part is one VGPR per chunk, so a copy costs almost no vector ALU work.
+//     Out-of-range rows read as zeros (the buffer bound is the (batch, head)
+//     slice);
+//   * the loop is software-pipelined: iteration c computes S for chunk c + 1
+//     on the matrix cores while the vector ALUs turn S of chunk c into
+//     probabilities, then accumulates P V of chunk c.  K runs two chunks
+//     ahead of V in the copies;
 //   * products use v_mfma_f32_32x32x16_bf16 in the transposed orientation
 //     (S^T = K Q^T, O^T = V^T P^T), so each lane holds 16 keys of one query
-//     per 32-key block and a row max or sum needs one exchange with lane ^ 32;
+//     per 32-key block and a row max or sum needs one exchange with lane ^ 32
+//     (v_permlane32_swap);
 //   * V^T operands come straight from the row-major V tile through
 //     ds_read_b64_tr_b16, which hands each lane 4 keys of one channel.
 //
@@ -48,14 +56,18 @@ typedef float floatx2 __attribute__((ext_vector_type(2)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef uint16_t u16;
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int D = 64;
 constexpr int KC = 64;                 // keys per chunk
 constexpr float kRescaleSlack = 8.0f;  // rescale only when the max grows by > 2^8
 constexpr int TILE_BYTES = KC * D * 2; // one K or V chunk in LDS (8 KB)
-// s_waitcnt immediate (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt
-// 6:4, lgkmcnt 11:8): wait for every outstanding vector memory operation.
+// s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt
+// 6:4, lgkmcnt 11:8): every vector memory operation done / every LDS done.
 constexpr int kWaitVm0 = 0x0F70;
+constexpr int kWaitLgkm0 = 0xC07F;
+// Buffer resource word 3 for raw (unformatted, unswizzled) dword access.
+constexpr int kRawBufferFlags = 0x00020000;
 
 // Where one workgroup's keys come from.
 struct Plan {
@@ -64,28 +76,38 @@ struct Plan {
   int natural_end;   // > 0: keys are rows [0, natural_end) in order
 };
 
-// Element offsets of the key rows this lane copies with DMA instructions
-// m = 4 w + mm (mm = 0..3) of one chunk: a wave-uniform base `ub` plus the
-// uniform per-instruction part `mu[mm]` and the per-lane part `lo` (always
-// non-negative).  The row of instruction m, lane l is key 8 m + l / 8.
-struct Rows {
-  int ub;
-  int mu[4];
-  unsigned lo;
+// Copy addresses of one chunk: instruction m (this wave issues m = 4 w ..
+// 4 w + 3), lane l copies key 8 m + l / 8 of the chunk from element row
+// row0 + m * step (+ wrap when y0 + m < 0: a block row above the grid wraps to
+// its bottom) and byte lane_off within that row's 8-key group, relative to
+// the (batch, head) slice.  Keys outside [lo, hi) of the chunk are masked.
+struct Chunk {
+  int row0, step, y0;
+  unsigned lane_off;
+  int lo, hi;
 };
 
-__device__ __forceinline__ float swap_max(float v) { return fmaxf(v, __shfl_xor(v, 32)); }
-__device__ __forceinline__ float swap_sum(float v) { return v + __shfl_xor(v, 32); }
+__device__ __forceinline__ float swap_max(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float swap_sum(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
 // Two fp32 -> two bf16 (round to nearest even) in one 32-bit word.
 __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2{lo, hi}, bf16x2));
 }
 
-__global__ void __launch_bounds__(128) k_attn_w64(AttnArgs a) {
+// DENSE: every group runs natural-order rows over all keys (no index).
+template <bool DENSE>
+__global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2)))
+k_attn_w64(AttnArgs a) {
   // Two buffers each for K and V, declared separately so every access names
-  // one buffer statically: the compiler can then tell that a read of chunk c
-  // does not overlap the copy of chunk c + 1 still in flight.
+  // one buffer statically: the compiler can then tell that a read of one
+  // chunk does not overlap the copy of another still in flight.
   __shared__ __attribute__((aligned(16))) char kA[TILE_BYTES];
   __shared__ __attribute__((aligned(16))) char kB[TILE_BYTES];
   __shared__ __attribute__((aligned(16))) char vA[TILE_BYTES];
@@ -123,14 +145,15 @@ __global__ void __launch_bounds__(128) k_attn_w64(AttnArgs a) {
   u16* obase = static_cast<u16*>(a.o) + off;
   const int st = (int)a.st;
 
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int hw = lane >> 5, l32 = lane & 31;
 
   Plan p;
   int qrow;
   int listv = -1;   // lane e holds kept block id number e (image groups)
-  if (r < a.n_text_groups) {   // natural order: text rows, or every row (dense)
-    const int end = a.dense ? a.seq : a.f.n_text;
+  if (DENSE || r < a.n_text_groups) {   // natural order: text rows, or every row
+    const int end = DENSE ? a.seq : a.f.n_text;
     const int q = r * 64 + 32 * w + l32;
     qrow = q < end ? q : -1;
     p.img_chunks = 0;
@@ -154,13 +177,20 @@ __global__ void __launch_bounds__(128) k_attn_w64(AttnArgs a) {
   for (int ks = 0; ks < 4; ++ks)
     qf[ks] = *reinterpret_cast<const bf16x8*>(qbase + max(qrow, 0) * st + 16 * ks + 8 * hw);
 
+  // Buffer resources over this (batch, head) slice: rows [0, seq).
+  const unsigned slice_bytes = 2u * (unsigned)((a.seq - 1) * st + D);
+  const __amdgpu_buffer_rsrc_t rk =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<u16*>(kbase), (short)0, (int)slice_bytes, kRawBufferFlags);
+  const __amdgpu_buffer_rsrc_t rv =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<u16*>(vbase), (short)0, (int)slice_bytes, kRawBufferFlags);
+
   // DMA lane mapping: lane l of instruction m fills key 8 m + l / 8, physical
   // chunk l % 8 -- logical K chunk (l % 8) ^ ((key >> 1) & 7) and logical V
   // chunk (l % 8) ^ (4 ((key >> 1) & 1)).  (key >> 1) & 7 = 4 (m & 1) + l / 16.
   const int vk = lane >> 3;
-  const int kcol0 = 8 * ((lane & 7) ^ (lane >> 4));         // m even
-  const int kcol1 = 8 * ((lane & 7) ^ (4 + (lane >> 4)));   // m odd
-  const int vcol = 8 * ((lane & 7) ^ (4 * ((lane >> 4) & 1)));
+  const unsigned kc0 = 16u * ((lane & 7) ^ (lane >> 4));          // bytes, m even
+  const unsigned kc1 = 16u * ((lane & 7) ^ (4 + (lane >> 4)));    // bytes, m odd
+  const unsigned vcb = 16u * ((lane & 7) ^ (4 * ((lane >> 4) & 1)));
   // K operand reads: key 32 kb + l32, logical chunk 2 ks + hw.
   const int g = (l32 >> 1) & 7;
   int koff[4];
@@ -183,52 +213,72 @@ __global__ void __launch_bounds__(128) k_attn_w64(AttnArgs a) {
     orig_x = (listv - ty * a.f.nx) * 8 - a.f.sx;
   }
 
-  // Rows of chunk c for this wave's four DMA instructions, and the range
-  // [lo, hi) of the chunk's 64 keys that are real.  Natural-order chunks
-  // always cover 64 existing rows: a ragged last chunk is moved back to end at
-  // the last row and masks the keys the previous chunk already covered (rows
-  // of a ragged text chunk that run into the image rows exist too).
-  auto rows_of = [&](int c, Rows& rw, int& lo, int& hi) {
-    if (c < p.img_chunks) {
+  // Addresses of chunk c.  Image chunks: block row m of the frame wraps to
+  // the bottom of the grid when it starts above it (a scalar correction), and
+  // each lane's column wraps to the right edge when it starts left of it.
+  // Natural-order chunks always cover 64 existing rows: a ragged last chunk
+  // is moved back to end at the last row and masks the keys the previous
+  // chunk already covered (rows of a ragged text chunk that run into the
+  // image rows exist too).
+  auto chunk_of = [&](int c) {
+    Chunk ch;
+    if (!DENSE && c < p.img_chunks) {
       const int j = __builtin_amdgcn_readlane(listv, c);
-      const int y0 = __builtin_amdgcn_readlane(orig_y, c);
       const int x0 = __builtin_amdgcn_readlane(orig_x, c);
-      rw.ub = (a.f.n_text + y0 * W + x0) * st;
-      const int x = x0 + vk;
-      rw.lo = vk * st + (x < 0 ? W * st : 0);
-#pragma unroll
-      for (int mm = 0; mm < 4; ++mm) {
-        const int m = 4 * w + mm;
-        rw.mu[mm] = m * W * st + (y0 + m < 0 ? H * W * st : 0);
-      }
-      lo = 0;
-      hi = j >= 0 ? KC : 0;
-      return;
+      ch.y0 = __builtin_amdgcn_readlane(orig_y, c);
+      ch.row0 = a.f.n_text + ch.y0 * W;
+      ch.step = W;
+      const unsigned x = (unsigned)(x0 + vk);
+      ch.lane_off = 2u * min(x, x + (unsigned)W) * (unsigned)st;   // x < 0 wraps by W
+      ch.lo = 0;
+      ch.hi = j >= 0 ? KC : 0;
+      return ch;
     }
     const int end = p.natural_end ? p.natural_end : a.f.n_text;
     int base = p.natural_end ? c * KC : (c - p.img_chunks) * KC;
-    lo = 0;
-    hi = min(end - base, KC);
-    if (hi < KC && end >= KC) {   // ragged last chunk: end it at the last row
-      lo = KC - hi;
-      hi = KC;
+    ch.lo = 0;
+    ch.hi = min(end - base, KC);
+    if (ch.hi < KC && end >= KC) {   // ragged last chunk: end it at the last row
+      ch.lo = KC - ch.hi;
+      ch.hi = KC;
       base = end - KC;
     }
-    rw.ub = base * st;
-    rw.lo = vk * st;
-#pragma unroll
-    for (int mm = 0; mm < 4; ++mm) rw.mu[mm] = 8 * (4 * w + mm) * st;
+    ch.row0 = base;
+    ch.step = 8;
+    ch.y0 = 0;
+    ch.lane_off = 2u * (unsigned)(vk * st);
+    return ch;
   };
+  const int wrap = H * W;
 
-  // This wave's half of chunk c: K and V instructions m = 4 w .. 4 w + 3.
-  auto issue = [&](const Rows& rw, char* kd, char* vd) {
+  // This wave's half of the K or V copy of a chunk.  The LDS base of the
+  // wave's rows is kept opaque so the per-instruction LDS addresses are
+  // formed with one scalar add each instead of being held in registers.
+  auto copy = [&](const __amdgpu_buffer_rsrc_t& rs, const Chunk& ch, char* dst, bool is_k) {
+    int wb = 4096 * w;
+    asm volatile("" : "+s"(wb));
 #pragma unroll
     for (int mm = 0; mm < 4; ++mm) {
       const int m = 4 * w + mm;
-      const unsigned o = rw.lo + (unsigned)rw.mu[mm];
-      __builtin_amdgcn_global_load_lds(kbase + rw.ub + o + ((mm & 1) ? kcol1 : kcol0),
-                                       kd + 1024 * m, 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(vbase + rw.ub + o + vcol, vd + 1024 * m, 16, 0, 0);
+      const int row = ch.row0 + m * ch.step + (ch.y0 + m < 0 ? wrap : 0);
+      const unsigned col = is_k ? ((mm & 1) ? kc1 : kc0) : vcb;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(dst + wb + 1024 * mm), 16,
+                                               ch.lane_off + col, 2u * (unsigned)row * (unsigned)st, 0, 0);
+    }
+  };
+  auto copy_k = [&](const Chunk& ch, char* dst) { copy(rk, ch, dst, true); };
+  auto copy_v = [&](const Chunk& ch, char* dst) { copy(rv, ch, dst, false); };
+
+  // S^T = K . Q^T for a 64-key chunk (keys 32 kb + 8 (r / 4) + 4 hw + r % 4).
+  auto scores = [&](const char* kt, floatx16 (&sc)[2]) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      sc[kb] = floatx16{};
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kt + 4096 * kb + koff[ks]);
+        sc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sc[kb], 0, 0, 0);
+      }
     }
   };
 
@@ -239,48 +289,22 @@ __global__ void __launch_bounds__(128) k_attn_w64(AttnArgs a) {
   const float c2 = a.scale_log2;
   const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
 
-  int lo_cur = 0, hi_cur = 0;
-  if (p.n_chunks > 0) {
-    Rows rw;
-    rows_of(0, rw, lo_cur, hi_cur);
-    issue(rw, kA, vA);
-  }
-  __builtin_amdgcn_s_waitcnt(kWaitVm0);
-  __syncthreads();
-
-  // Chunk c from buffers (kt, vt); chunk c + 1 is copied into (kn, vn).
-  auto body = [&](int c, const char* kt, const char* vt, char* kn, char* vn) {
-
-    // S^T[kb] = K_kb . Q^T  (keys 32 kb + 8 (r / 4) + 4 hw + r % 4)
-    floatx16 sc[2];
+  // Masks the keys of a chunk outside [lo, hi) (rare: ragged or invalid).
+  auto mask = [&](floatx16 (&sc)[2], int lo, int hi) {
+    int l4 = lo - 4 * hw, h4 = hi - 4 * hw;
+    asm volatile("" : "+v"(l4), "+v"(h4));
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      sc[kb] = floatx16{};
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kt + 4096 * kb + koff[ks]);
-        sc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sc[kb], 0, 0, 0);
+      for (int rr = 0; rr < 16; ++rr) {
+        const int key = 32 * kb + 8 * (rr >> 2) + (rr & 3);   // minus 4 * hw
+        if (key < l4 || key >= h4) sc[kb][rr] = -INFINITY;
       }
-    }
-    const int lo = lo_cur, hi = hi_cur;
-    if (c + 1 < p.n_chunks) {   // start chunk c + 1 into the other buffers
-      Rows rw;
-      rows_of(c + 1, rw, lo_cur, hi_cur);
-      issue(rw, kn, vn);
-    }
+  };
 
-    if (lo > 0 || hi < KC) {   // rare: ragged chunk or invalid block id
-      int l4 = lo - 4 * hw, h4 = hi - 4 * hw;
-      asm volatile("" : "+v"(l4), "+v"(h4));
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int rr = 0; rr < 16; ++rr) {
-          const int key = 32 * kb + 8 * (rr >> 2) + (rr & 3);   // minus 4 * hw
-          if (key < l4 || key >= h4) sc[kb][rr] = -INFINITY;
-        }
-    }
-    // Online softmax (log2 domain, lazy rescale).
+  // Running max update for a chunk's scores; rescales O and l when the max
+  // grows by more than the slack.
+  auto update_max = [&](const floatx16 (&sc)[2]) {
     float mx = fmaxf(sc[0][0], sc[1][0]);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -296,8 +320,14 @@ __global__ void __launch_bounds__(128) k_attn_w64(AttnArgs a) {
       oacc[0] *= alpha;
       oacc[1] *= alpha;
     }
+  };
+
+  // P = exp2(c2 S - m) as bf16 pairs; l += row sums of the rounded P;
+  // O^T += V^T . P^T over 4 key steps of 16 (V^T operands: keys
+  // 16 ks + 8 (e / 4) + 4 hw + e % 4, channel 32 db + lane % 32).
+  auto probs_pv = [&](const floatx16 (&sc)[2], const char* vt) {
     const float mneg = -m_run;
-    uint32_t pk[2][8];   // [kb] bf16 pairs of the lane's 16 probabilities
+    uint32_t pk[2][8];
     float ls0 = 0.f, ls1 = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -311,9 +341,6 @@ __global__ void __launch_bounds__(128) k_attn_w64(AttnArgs a) {
         else        ls0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wd), one2, ls0, false);
       }
     l_run += ls0 + ls1;
-
-    // O^T[db] += V^T . P^T over 4 key steps of 16.  V^T operands: keys
-    // 16 ks + 8 (e / 4) + 4 hw + e % 4, channel 32 db + lane % 32.
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       const uint32_t* wd = &pk[ks >> 1][4 * (ks & 1)];
@@ -326,15 +353,77 @@ __global__ void __launch_bounds__(128) k_attn_w64(AttnArgs a) {
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, v8), pb, oacc[db], 0, 0, 0);
       }
     }
+  };
 
-    // Chunk c + 1 has landed (this wave's half) and both waves are past their
-    // reads of chunk c before either starts chunk c + 2 into the same buffer.
+  const int n = p.n_chunks;
+  floatx16 sA[2], sB[2];   // scores of chunk c and c + 1, alternating roles
+  Chunk ch1;            // addresses of chunk c + 1 (its V is copied in iteration c)
+  int lo_c = 0, hi_c = 0, lo_n = 0, hi_n = 0;   // masks of chunks c and c + 1
+  if (n > 0) {
+    const Chunk ch0 = chunk_of(0);
+    copy_k(ch0, kA);
+    copy_v(ch0, vA);
+    lo_c = ch0.lo;
+    hi_c = ch0.hi;
+    if (n > 1) {
+      ch1 = chunk_of(1);
+      copy_k(ch1, kB);
+      lo_n = ch1.lo;
+      hi_n = ch1.hi;
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(kWaitVm0);
+  __syncthreads();
+  if (n > 0) scores(kA, sA);
+  // Both waves' reads of K(0) are done before K(2) is copied over it.
+  __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+  __syncthreads();
+
+  // Iteration c: scores of chunk c in sc, K(c + 1) in kr, V(c) in vr; the
+  // scores of chunk c + 1 go to sn.  K(c + 2) is copied into kw (where K(c)
+  // was) and V(c + 1) into vw (where V(c - 1) was).
+  auto body = [&](int c, floatx16 (&sc)[2], floatx16 (&sn)[2], const char* kr, const char* vr,
+                  char* kw, char* vw) {
+    if (c + 2 < n) {
+      const Chunk ch2 = chunk_of(c + 2);
+      copy_k(ch2, kw);
+      copy_v(ch1, vw);
+      ch1 = ch2;
+    } else {
+      copy_v(ch1, vw);
+    }
+    if (lo_c > 0 || hi_c < KC) mask(sc, lo_c, hi_c);
+    update_max(sc);
+    scores(kr, sn);
+    probs_pv(sc, vr);
+    lo_c = lo_n;
+    hi_c = hi_n;
+    lo_n = ch1.lo;
+    hi_n = ch1.hi;
+    // Copies issued above have landed (this wave's half) and both waves are
+    // past their reads of kr and vr before either copies into them.
     __builtin_amdgcn_s_waitcnt(kWaitVm0);
     __syncthreads();
   };
-  for (int c = 0; c < p.n_chunks; c += 2) {
-    body(c, kA, vA, kB, vB);
-    if (c + 1 < p.n_chunks) body(c + 1, kB, vB, kA, vA);
+  // body(c) runs only while chunk c + 1 exists; the last chunk is finished
+  // without next scores or copies.
+  int c = 0;
+  for (; c + 2 < n; c += 2) {
+    body(c, sA, sB, kB, vA, kA, vB);
+    body(c + 1, sB, sA, kA, vB, kB, vA);
+  }
+  if (c + 1 < n) {
+    body(c, sA, sB, kB, vA, kA, vB);
+    ++c;
+  }
+  auto last = [&](floatx16 (&sc)[2], const char* vr) {
+    if (lo_c > 0 || hi_c < KC) mask(sc, lo_c, hi_c);
+    update_max(sc);
+    probs_pv(sc, vr);
+  };
+  if (c < n) {
+    if (c & 1) last(sB, vB);
+    else last(sA, vA);
   }
 
   // Epilogue: O = O^T / l, 4 consecutive channels per store.
@@ -355,8 +444,10 @@ __global__ void __launch_bounds__(128) k_attn_w64(AttnArgs a) {
 
 }  // namespace
 
+const char* w64_kernel_name(bool dense) { return dense ? "k_attn_w64<true>" : "k_attn_w64<false>"; }
+
 bool w64_supported(int head_dim, int tile, bool dense, int n_tiles, int seq, int64_t span) {
-  // 32-bit element offsets inside one (batch, head); at most 64 kept blocks;
+  // 32-bit byte offsets inside one (batch, head); at most 64 kept blocks;
   // natural-order chunks need at least one full chunk of rows.
   return head_dim == 64 && (dense || (tile == 8 && n_tiles <= 64)) && seq >= KC &&
          span < ((int64_t)1 << 31);
@@ -375,7 +466,10 @@ hipError_t launch_attn_w64(const AttnArgs& a0, hipStream_t s) {
   }
   const int64_t total = (int64_t)a.batch * a.heads * a.groups_per_bh;
   if (total <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_attn_w64, dim3((unsigned)total), dim3(128), 0, s, a);
+  if (a.dense)
+    hipLaunchKernelGGL(k_attn_w64<true>, dim3((unsigned)total), dim3(128), 0, s, a);
+  else
+    hipLaunchKernelGGL(k_attn_w64<false>, dim3((unsigned)total), dim3(128), 0, s, a);
   return hipGetLastError();
 }
 

@@ -112,3 +112,21 @@ def test_misaligned_pointers_rejected(lib):
     # bf16 attention needs 16-byte aligned bases; rejected before any launch.
     assert _lib.forward(d, 0x1002, 0x2000, 0x3000, 0x4000, 0x5000, None) == _lib.SSBA_ERR_ARG
     assert _lib.build_index(d, 0x1000, 0x2000, 0x3002, 0x4000, None) == _lib.SSBA_ERR_ARG
+
+
+@pytest.mark.parametrize("kw,dense,name", [
+    ({}, False, "k_attn_w64<false>"),
+    ({}, True, "k_attn_w64<true>"),
+    ({"n_text": 256, "batch": 2, "heads": 24}, False, "k_attn_w64<false>"),
+    ({"grid_h": 128, "grid_w": 128, "tile": 16, "head_dim": 128, "keep": 7}, False, "k_attn_bf16<128, 4>"),
+    ({"grid_h": 16, "grid_w": 16, "tile": 4, "keep": 4, "dtype": _lib.DT_F32}, False, "k_attn_f32<64>"),
+    ({"grid_h": 32, "grid_w": 32, "tile": 4, "keep": 4}, False, "k_attn_bf16<64, 2>"),
+])
+def test_forward_kernel_names(lib, kw, dense, name):
+    assert _lib.forward_kernel(_desc(**kw), dense) == name
+
+
+def test_forward_kernel_name_of_invalid_descriptor(lib):
+    assert _lib.forward_kernel(_desc(keep=0)) is None
+    assert _lib.forward_kernel(_desc(keep=0), dense=True) == "k_attn_w64<true>"
+    assert _lib.forward_kernel(_desc(head_dim=96)) is None
