@@ -5,7 +5,11 @@
 
 One step = one SSBA layer call on inputs already resident in HBM: the top-k
 gate (block pooling, affinity, ranking -> index) followed by the block-sparse
-attention kernel.  Prints ONE JSON line on stdout; --sweep prints extra
+attention kernel.  Steps run back to back between two HIP events on the
+stream the library launches on, once launched eagerly and once replayed from
+a HIP graph captured from the same calls (same kernels, same work; the replay
+is checked bit-exact against the eager output); `value` uses the faster.
+Index, forward and dense launches are also timed separately, back to back.  Prints ONE JSON line on stdout; --sweep prints extra
 per-configuration lines on stderr (sparsity sweep, text tokens, 2K grid).
 
 Flops are counted over computed (kept) query/key pairs only: 4 * D per pair
@@ -119,37 +123,52 @@ class Runner:
         self.ssba.build_index(self.q, self.k, self.desc, self.index, self.scratch)
         self.ssba.forward(self.q, self.k, self.v, self.index, self.desc, self.out)
 
-    def timed_steps(self, steps: int):
-        """Events around each launch of `steps` back-to-back steps."""
-        torch = self.torch
-        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for e in ev:
-            e[0].record()
-            self.ssba.build_index(self.q, self.k, self.desc, self.index, self.scratch)
-            e[1].record()
-            self.ssba.forward(self.q, self.k, self.v, self.index, self.desc, self.out)
-            e[2].record()
-        torch.cuda.synchronize()
-        wall = time.perf_counter() - t0
-        idx_ms = [e[0].elapsed_time(e[1]) for e in ev]
-        fwd_ms = [e[1].elapsed_time(e[2]) for e in ev]
-        span_ms = ev[0][0].elapsed_time(ev[-1][2])
-        return wall * 1e3 / steps, span_ms / steps, float(np.mean(idx_ms)), float(np.mean(fwd_ms))
-
-    def timed_dense(self, steps: int) -> float:
+    def _span(self, fn, steps: int) -> float:
+        """Milliseconds per call of `fn`: HIP events on the current stream (the
+        one the library launches on) around `steps` back-to-back calls."""
         torch = self.torch
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        for _ in range(3):
-            self.ssba.forward_dense(self.q, self.k, self.v, self.desc, self.out_dense)
         torch.cuda.synchronize()
         e0.record()
         for _ in range(steps):
-            self.ssba.forward_dense(self.q, self.k, self.v, self.desc, self.out_dense)
+            fn()
         e1.record()
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / steps
+
+    def run_index(self):
+        self.ssba.build_index(self.q, self.k, self.desc, self.index, self.scratch)
+
+    def run_fwd(self):
+        self.ssba.forward(self.q, self.k, self.v, self.index, self.desc, self.out)
+
+    def run_dense(self):
+        self.ssba.forward_dense(self.q, self.k, self.v, self.desc, self.out_dense)
+
+    def timed_steps(self, steps: int):
+        """Whole steps (index + forward) back to back: wall ms and event ms per step."""
+        torch = self.torch
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ms = self._span(self.step, steps)
+        wall = (time.perf_counter() - t0) * 1e3 / steps
+        return wall, ms
+
+    def graph_step_ms(self, steps: int):
+        """The same step captured once in a HIP graph and replayed."""
+        torch = self.torch
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for _ in range(3):
+                self.step()
+        torch.cuda.current_stream().wait_stream(side)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            self.step()
+        g.replay()
+        ms = self._span(g.replay, steps)
+        return ms, g
 
 
 def cpu_baseline(runner, budget_s: float = 12.0) -> dict:
@@ -191,20 +210,35 @@ def cpu_baseline(runner, budget_s: float = 12.0) -> dict:
             "seconds": round(t_index + t_attn, 3)}
 
 
-def measure(w, steps: int, warmup: int, dense_steps: int):
+def measure(w, steps: int, warmup: int, dense_steps: int, graph: bool = True):
     r = Runner(w)
     for _ in range(warmup):
         r.step()
-    wall_ms, step_ms, idx_ms, fwd_ms = r.timed_steps(steps)
-    dense_ms = r.timed_dense(dense_steps)
+    wall_ms, step_ms = r.timed_steps(steps)
+    idx_ms = r._span(r.run_index, steps)
+    fwd_ms = r._span(r.run_fwd, steps)
+    for _ in range(3):
+        r.run_dense()
+    dense_ms = r._span(r.run_dense, dense_steps)
+    graph_ms = None
+    if graph:
+        graph_ms, g = r.graph_step_ms(steps)
+        # the graph's outputs must equal the eager ones bit for bit
+        ref = r.out.clone()
+        g.replay()
+        r.torch.cuda.synchronize()
+        assert r.torch.equal(ref, r.out), "graph replay differs from eager step"
+        del g
+    best_ms = min(step_ms, graph_ms) if graph_ms is not None else step_ms
     f = flops(w)
     return r, {
-        "ms_step_wall": wall_ms, "ms_step": step_ms, "ms_index": idx_ms, "ms_fwd": fwd_ms,
+        "ms_step_wall": wall_ms, "ms_step_eager": step_ms, "ms_step_graph": graph_ms,
+        "ms_step": best_ms, "ms_index": idx_ms, "ms_fwd": fwd_ms,
         "ms_dense": dense_ms, "gflop": f / 1e9, "gflop_dense": flops(w, dense=True) / 1e9,
         "tflops_fwd": f / (fwd_ms * 1e-3) / 1e12,
-        "tflops_step": f / (step_ms * 1e-3) / 1e12,
+        "tflops_step": f / (best_ms * 1e-3) / 1e12,
         "tflops_dense": flops(w, dense=True) / (dense_ms * 1e-3) / 1e12,
-        "speedup_kernel": dense_ms / fwd_ms, "speedup_step": dense_ms / step_ms,
+        "speedup_kernel": dense_ms / fwd_ms, "speedup_step": dense_ms / best_ms,
     }
 
 
@@ -257,6 +291,8 @@ def main():
                    "seq_len": w.seq_len, "parallelism": "none (1 GPU)"},
         "ms_fwd": round(m["ms_fwd"], 5), "ms_index": round(m["ms_index"], 5),
         "ms_dense": round(m["ms_dense"], 5), "ms_step_wall": round(m["ms_step_wall"], 5),
+        "ms_step_eager": round(m["ms_step_eager"], 5),
+        "ms_step_graph": None if m["ms_step_graph"] is None else round(m["ms_step_graph"], 5),
         "tflops_fwd": round(m["tflops_fwd"], 2), "pct_peak_fwd": round(100 * m["tflops_fwd"] / PEAK_BF16_TFLOPS, 2),
         "tflops_dense": round(m["tflops_dense"], 2),
         "speedup_vs_dense_kernel": round(m["speedup_kernel"], 3),
@@ -273,9 +309,9 @@ def main():
         for c in cases:
             del r
             torch.cuda.empty_cache()
-            r, mm = measure(c, max(20, args.steps // 2), 5, 20)
+            r, mm = measure(c, max(20, args.steps // 2), 5, 20, graph=False)
             print(json.dumps({"workload": c.name, "desc": describe(c),
-                              **{k: round(v, 5) for k, v in mm.items()},
+                              **{k: (None if v is None else round(v, 5)) for k, v in mm.items()},
                               "pct_peak_fwd": round(100 * mm["tflops_fwd"] / PEAK_BF16_TFLOPS, 2)}),
                   file=sys.stderr, flush=True)
 

@@ -5,24 +5,26 @@
 // dense control).  Computes the attend step of Algorithm 1 like the generic
 // kernel; it differs only in how data reaches the matrix cores.
 //
-// At head_dim 64 the softmax of a 64x64 block pair costs as many VALU cycles
-// as its two products cost MFMA cycles, so the kernel is built to overlap
-// them:
-//   * a workgroup owns the 64 query rows of one block; its two waves take 32
-//     rows each;
-//   * every 64-key chunk of K and V is copied once per workgroup, by DMA
-//     (buffer_load_dwordx4 ... lds; each wave moves half of it), into
+// At head_dim 64 the softmax of a block pair costs as many VALU cycles as its
+// two products cost MFMA cycles, so the kernel is built for overlap between
+// waves:
+//   * a workgroup owns the 64 query rows of one block with four waves: wave w
+//     takes queries 32 (w % 2) .. + 31 and the keys 32 (w / 2) .. + 31 of every
+//     64-key chunk (one 8x4 half of a kept block), so each SIMD holds four
+//     waves; the two key streams are merged once at the end;
+//   * every 32-key half chunk of K and V is copied once per workgroup, by DMA
+//     (buffer_load_dwordx4 ... lds; the two waves of a stream split it), into
 //     double-buffered LDS.  Row offsets are scalar operands and the per-lane
 //     part is one VGPR per chunk, so a copy costs almost no vector ALU work.
 //     Out-of-range rows read as zeros (the buffer bound is the (batch, head)
 //     slice);
-//   * the loop is software-pipelined: iteration c computes S for chunk c + 1
-//     on the matrix cores while the vector ALUs turn S of chunk c into
-//     probabilities, then accumulates P V of chunk c.  K runs two chunks
-//     ahead of V in the copies;
+//   * the softmax is optimistic: probabilities are taken against the running
+//     max; only when a lane's chunk sum exceeds 2^20 (the max grew, or the
+//     first chunk) is the chunk max taken, O and l rescaled and the chunk
+//     redone, so the common chunk needs no max reduction;
 //   * products use v_mfma_f32_32x32x16_bf16 in the transposed orientation
 //     (S^T = K Q^T, O^T = V^T P^T), so each lane holds 16 keys of one query
-//     per 32-key block and a row max or sum needs one exchange with lane ^ 32
+//     and a row max or sum needs one exchange with lane ^ 32
 //     (v_permlane32_swap);
 //   * V^T operands come straight from the row-major V tile through
 //     ds_read_b64_tr_b16, which hands each lane 4 keys of one channel.
@@ -36,7 +38,7 @@
 // for element e: exactly the lane's own probabilities, so P^T never leaves
 // its registers.
 //
-// LDS tiles are 64 rows (keys) of 128 bytes.  A 16-byte column chunk c of key
+// LDS tiles are 32 rows (keys) of 128 bytes.  A 16-byte column chunk c of key
 // k sits at chunk c ^ ((k >> 1) & 7) in the K tile and c ^ (4 ((k >> 1) & 1))
 // in the V tile; with these swizzles the K operand reads (ds_read_b128), the
 // V transposing reads and the DMA writes all spread evenly over the banks.
@@ -59,13 +61,13 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int D = 64;
-constexpr int KC = 64;                 // keys per chunk
-constexpr float kRescaleSlack = 8.0f;  // rescale only when the max grows by > 2^8
-constexpr int TILE_BYTES = KC * D * 2; // one K or V chunk in LDS (8 KB)
+constexpr int KC = 64;                 // keys per chunk (one 8x8 block)
+constexpr int KH = 32;                 // keys per stream and chunk
+constexpr int HALF_BYTES = KH * D * 2; // one K or V half chunk in LDS (4 KB)
+constexpr float kSumLimit = 1048576.0f;   // 2^20: redo a chunk above this lane sum
 // s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt
-// 6:4, lgkmcnt 11:8): every vector memory operation done / every LDS done.
+// 6:4, lgkmcnt 11:8): every vector memory operation done.
 constexpr int kWaitVm0 = 0x0F70;
-constexpr int kWaitLgkm0 = 0xC07F;
 // Buffer resource word 3 for raw (unformatted, unswizzled) dword access.
 constexpr int kRawBufferFlags = 0x00020000;
 
@@ -76,11 +78,12 @@ struct Plan {
   int natural_end;   // > 0: keys are rows [0, natural_end) in order
 };
 
-// Copy addresses of one chunk: instruction m (this wave issues m = 4 w ..
-// 4 w + 3), lane l copies key 8 m + l / 8 of the chunk from element row
-// row0 + m * step (+ wrap when y0 + m < 0: a block row above the grid wraps to
-// its bottom) and byte lane_off within that row's 8-key group, relative to
-// the (batch, head) slice.  Keys outside [lo, hi) of the chunk are masked.
+// Copy addresses of this stream's half of one chunk: copy instruction m
+// (0..3; the wave issues two of them) lane l moves key 8 m + l / 8 of the
+// half from element row row0 + m * step (+ wrap when y0 + m < 0: a block row
+// above the grid wraps to its bottom) and byte lane_off within that row's
+// 8-key group, relative to the (batch, head) slice.  Keys outside [lo, hi)
+// of the half are masked.
 struct Chunk {
   int row0, step, y0;
   unsigned lane_off;
@@ -103,15 +106,16 @@ __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
 
 // DENSE: every group runs natural-order rows over all keys (no index).
 template <bool DENSE>
-__global__ void __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4)))
 k_attn_w64(AttnArgs a) {
-  // Two buffers each for K and V, declared separately so every access names
-  // one buffer statically: the compiler can then tell that a read of one
-  // chunk does not overlap the copy of another still in flight.
-  __shared__ __attribute__((aligned(16))) char kA[TILE_BYTES];
-  __shared__ __attribute__((aligned(16))) char kB[TILE_BYTES];
-  __shared__ __attribute__((aligned(16))) char vA[TILE_BYTES];
-  __shared__ __attribute__((aligned(16))) char vB[TILE_BYTES];
+  // K and V buffers A and B (alternate chunks); stream s uses bytes
+  // [4096 s, 4096 s + 4096) of each.  Declared separately so every access
+  // names one buffer statically: the compiler can then tell that a read of
+  // one chunk does not overlap the copy of the next still in flight.
+  __shared__ __attribute__((aligned(16))) char kA[2 * HALF_BYTES];
+  __shared__ __attribute__((aligned(16))) char kB[2 * HALF_BYTES];
+  __shared__ __attribute__((aligned(16))) char vA[2 * HALF_BYTES];
+  __shared__ __attribute__((aligned(16))) char vB[2 * HALF_BYTES];
 
   // Logical group id.  Consecutive hardware ids go round-robin over the 8
   // XCDs; when the (batch, head) count divides by 8 each XCD gets whole
@@ -147,6 +151,8 @@ k_attn_w64(AttnArgs a) {
 
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int qh = w & 1;    // query half
+  const int sk = w >> 1;   // key stream: keys 32 sk .. 32 sk + 31 of each chunk
   const int hw = lane >> 5, l32 = lane & 31;
 
   Plan p;
@@ -154,14 +160,14 @@ k_attn_w64(AttnArgs a) {
   int listv = -1;   // lane e holds kept block id number e (image groups)
   if (DENSE || r < a.n_text_groups) {   // natural order: text rows, or every row
     const int end = DENSE ? a.seq : a.f.n_text;
-    const int q = r * 64 + 32 * w + l32;
+    const int q = r * 64 + 32 * qh + l32;
     qrow = q < end ? q : -1;
     p.img_chunks = 0;
     p.natural_end = a.seq;
     p.n_chunks = (a.seq + KC - 1) / KC;
   } else {
     const int i = r - a.n_text_groups;
-    qrow = frame_row(a.f, i, 32 * w + l32);
+    qrow = frame_row(a.f, i, 32 * qh + l32);
     const int32_t* list = a.index + (bh * (int64_t)a.n_tiles + i) * (a.n_tiles + 1);
     const int count = min(max(list[0], 0), min(a.n_tiles, 64));
     const int e = lane < count ? list[1 + lane] : 0;
@@ -171,7 +177,7 @@ k_attn_w64(AttnArgs a) {
     p.n_chunks = p.img_chunks + (a.f.n_text + KC - 1) / KC;
   }
 
-  // Q^T operand [ks]: query 32 w + l32, channels 16 ks + 8 hw + [0, 8).
+  // Q^T operand [ks]: query 32 qh + l32, channels 16 ks + 8 hw + [0, 8).
   bf16x8 qf[4];
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks)
@@ -184,25 +190,27 @@ k_attn_w64(AttnArgs a) {
   const __amdgpu_buffer_rsrc_t rv =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<u16*>(vbase), (short)0, (int)slice_bytes, kRawBufferFlags);
 
-  // DMA lane mapping: lane l of instruction m fills key 8 m + l / 8, physical
-  // chunk l % 8 -- logical K chunk (l % 8) ^ ((key >> 1) & 7) and logical V
-  // chunk (l % 8) ^ (4 ((key >> 1) & 1)).  (key >> 1) & 7 = 4 (m & 1) + l / 16.
+  // DMA lane mapping: lane l of instruction m fills key 8 m + l / 8 of the
+  // half, physical chunk l % 8 -- logical K chunk (l % 8) ^ ((key >> 1) & 7)
+  // and logical V chunk (l % 8) ^ (4 ((key >> 1) & 1)), where
+  // (key >> 1) & 7 = 4 (m & 1) + l / 16.
   const int vk = lane >> 3;
   const unsigned kc0 = 16u * ((lane & 7) ^ (lane >> 4));          // bytes, m even
   const unsigned kc1 = 16u * ((lane & 7) ^ (4 + (lane >> 4)));    // bytes, m odd
   const unsigned vcb = 16u * ((lane & 7) ^ (4 * ((lane >> 4) & 1)));
-  // K operand reads: key 32 kb + l32, logical chunk 2 ks + hw.
+  // K operand reads: key l32, logical chunk 2 ks + hw.
   const int g = (l32 >> 1) & 7;
   int koff[4];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) koff[ks] = l32 * 128 + 16 * ((2 * ks + hw) ^ g);
+  for (int ks = 0; ks < 4; ++ks) koff[ks] = HALF_BYTES * sk + l32 * 128 + 16 * ((2 * ks + hw) ^ g);
   // V transposing reads: 16-lane group G = lane / 16, i = lane % 16 points at
   // key 16 ks + 8 r' + 4 hw + i / 4, channels 32 db + 16 (G % 2) + 4 (i % 4).
   const int G = lane >> 4, li = lane & 15;
   int voff[2];
 #pragma unroll
   for (int db = 0; db < 2; ++db)
-    voff[db] = (4 * hw + (li >> 2)) * 128 + 64 * (db ^ ((li >> 3) & 1)) + 32 * (G & 1) + 8 * (li & 3);
+    voff[db] = HALF_BYTES * sk + (4 * hw + (li >> 2)) * 128 + 64 * (db ^ ((li >> 3) & 1)) +
+               32 * (G & 1) + 8 * (li & 3);
 
   // Frame origin (y0, x0) of each kept block, one block per lane.
   const int W = a.f.grid_w, H = a.f.grid_h;
@@ -213,8 +221,7 @@ k_attn_w64(AttnArgs a) {
     orig_x = (listv - ty * a.f.nx) * 8 - a.f.sx;
   }
 
-  // Addresses of chunk c.  Image chunks: block row m of the frame wraps to
-  // the bottom of the grid when it starts above it (a scalar correction), and
+  // This stream's half of chunk c.  Image chunks: block rows 4 sk .. 4 sk + 3;
   // each lane's column wraps to the right edge when it starts left of it.
   // Natural-order chunks always cover 64 existing rows: a ragged last chunk
   // is moved back to end at the last row and masks the keys the previous
@@ -225,25 +232,26 @@ k_attn_w64(AttnArgs a) {
     if (!DENSE && c < p.img_chunks) {
       const int j = __builtin_amdgcn_readlane(listv, c);
       const int x0 = __builtin_amdgcn_readlane(orig_x, c);
-      ch.y0 = __builtin_amdgcn_readlane(orig_y, c);
+      ch.y0 = __builtin_amdgcn_readlane(orig_y, c) + 4 * sk;
       ch.row0 = a.f.n_text + ch.y0 * W;
       ch.step = W;
       const unsigned x = (unsigned)(x0 + vk);
       ch.lane_off = 2u * min(x, x + (unsigned)W) * (unsigned)st;   // x < 0 wraps by W
       ch.lo = 0;
-      ch.hi = j >= 0 ? KC : 0;
+      ch.hi = j >= 0 ? KH : 0;
       return ch;
     }
     const int end = p.natural_end ? p.natural_end : a.f.n_text;
     int base = p.natural_end ? c * KC : (c - p.img_chunks) * KC;
-    ch.lo = 0;
-    ch.hi = min(end - base, KC);
-    if (ch.hi < KC && end >= KC) {   // ragged last chunk: end it at the last row
-      ch.lo = KC - ch.hi;
-      ch.hi = KC;
+    int lo = 0, hi = min(end - base, KC);
+    if (hi < KC && end >= KC) {   // ragged last chunk: end it at the last row
+      lo = KC - hi;
+      hi = KC;
       base = end - KC;
     }
-    ch.row0 = base;
+    ch.lo = min(max(lo - KH * sk, 0), KH);
+    ch.hi = min(max(hi - KH * sk, 0), KH);
+    ch.row0 = base + KH * sk;
     ch.step = 8;
     ch.y0 = 0;
     ch.lane_off = 2u * (unsigned)(vk * st);
@@ -251,34 +259,19 @@ k_attn_w64(AttnArgs a) {
   };
   const int wrap = H * W;
 
-  // This wave's half of the K or V copy of a chunk.  The LDS base of the
-  // wave's rows is kept opaque so the per-instruction LDS addresses are
-  // formed with one scalar add each instead of being held in registers.
+  // This wave's two of the four copy instructions of a half chunk, into
+  // the stream's 4 KB of buffer `dst`.  The LDS base is kept opaque so each
+  // instruction's LDS address is one scalar add rather than a held register.
   auto copy = [&](const __amdgpu_buffer_rsrc_t& rs, const Chunk& ch, char* dst, bool is_k) {
-    int wb = 4096 * w;
-    asm volatile("" : "+s"(wb));
+    int lb = HALF_BYTES * sk + 2048 * qh;
+    asm volatile("" : "+s"(lb));
 #pragma unroll
-    for (int mm = 0; mm < 4; ++mm) {
-      const int m = 4 * w + mm;
+    for (int mm = 0; mm < 2; ++mm) {
+      const int m = 2 * qh + mm;
       const int row = ch.row0 + m * ch.step + (ch.y0 + m < 0 ? wrap : 0);
       const unsigned col = is_k ? ((mm & 1) ? kc1 : kc0) : vcb;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(dst + wb + 1024 * mm), 16,
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(dst + lb + 1024 * mm), 16,
                                                ch.lane_off + col, 2u * (unsigned)row * (unsigned)st, 0, 0);
-    }
-  };
-  auto copy_k = [&](const Chunk& ch, char* dst) { copy(rk, ch, dst, true); };
-  auto copy_v = [&](const Chunk& ch, char* dst) { copy(rv, ch, dst, false); };
-
-  // S^T = K . Q^T for a 64-key chunk (keys 32 kb + 8 (r / 4) + 4 hw + r % 4).
-  auto scores = [&](const char* kt, floatx16 (&sc)[2]) {
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      sc[kb] = floatx16{};
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kt + 4096 * kb + koff[ks]);
-        sc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sc[kb], 0, 0, 0);
-      }
     }
   };
 
@@ -289,62 +282,62 @@ k_attn_w64(AttnArgs a) {
   const float c2 = a.scale_log2;
   const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
 
-  // Masks the keys of a chunk outside [lo, hi) (rare: ragged or invalid).
-  auto mask = [&](floatx16 (&sc)[2], int lo, int hi) {
-    int l4 = lo - 4 * hw, h4 = hi - 4 * hw;
-    asm volatile("" : "+v"(l4), "+v"(h4));
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int rr = 0; rr < 16; ++rr) {
-        const int key = 32 * kb + 8 * (rr >> 2) + (rr & 3);   // minus 4 * hw
-        if (key < l4 || key >= h4) sc[kb][rr] = -INFINITY;
-      }
-  };
-
-  // Running max update for a chunk's scores; rescales O and l when the max
-  // grows by more than the slack.
-  auto update_max = [&](const floatx16 (&sc)[2]) {
-    float mx = fmaxf(sc[0][0], sc[1][0]);
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int rr = 0; rr < 16; ++rr) mx = fmaxf(mx, sc[kb][rr]);
-    mx = swap_max(mx) * c2;
-    const bool grow = mx > m_run + kRescaleSlack;
-    if (__any(grow)) {
-      const float m_new = grow ? mx : m_run;
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
-      l_run *= alpha;
-      oacc[0] *= alpha;
-      oacc[1] *= alpha;
-    }
-  };
-
-  // P = exp2(c2 S - m) as bf16 pairs; l += row sums of the rounded P;
-  // O^T += V^T . P^T over 4 key steps of 16 (V^T operands: keys
-  // 16 ks + 8 (e / 4) + 4 hw + e % 4, channel 32 db + lane % 32).
-  auto probs_pv = [&](const floatx16 (&sc)[2], const char* vt) {
-    const float mneg = -m_run;
-    uint32_t pk[2][8];
-    float ls0 = 0.f, ls1 = 0.f;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int rr = 0; rr < 16; rr += 2) {
-        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[kb][rr], c2, mneg));
-        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[kb][rr + 1], c2, mneg));
-        const uint32_t wd = pack2(p0, p1);
-        pk[kb][rr >> 1] = wd;
-        if (rr & 2) ls1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wd), one2, ls1, false);
-        else        ls0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, wd), one2, ls0, false);
-      }
-    l_run += ls0 + ls1;
+  // One half chunk: K in kt, V in vt (this stream's halves), keys outside
+  // [lo, hi) masked.
+  auto step = [&](const char* kt, const char* vt, int lo, int hi) {
+    // S^T = K . Q^T: the lane's 16 keys 8 (r / 4) + 4 hw + r % 4 of its query.
+    floatx16 sc = floatx16{};
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      const uint32_t* wd = &pk[ks >> 1][4 * (ks & 1)];
-      const bf16x8 pb = __builtin_bit_cast(bf16x8, make_uint4(wd[0], wd[1], wd[2], wd[3]));
+      const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kt + koff[ks]);
+      sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sc, 0, 0, 0);
+    }
+    if (lo > 0 || hi < KH) {   // rare: ragged chunk or invalid block id
+      int l4 = lo - 4 * hw, h4 = hi - 4 * hw;
+      asm volatile("" : "+v"(l4), "+v"(h4));
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) {
+        const int key = 8 * (rr >> 2) + (rr & 3);   // minus 4 * hw
+        if (key < l4 || key >= h4) sc[rr] = -INFINITY;
+      }
+    }
+    // P = exp2(c2 S - m) as bf16 pairs and the lane's sum of the rounded P.
+    uint32_t pk[8];
+    float ls;
+    auto probs = [&]() {
+      const float mneg = -m_run;
+      float ls0 = 0.f, ls1 = 0.f;
+#pragma unroll
+      for (int rr = 0; rr < 16; rr += 2) {
+        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[rr], c2, mneg));
+        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[rr + 1], c2, mneg));
+        pk[rr >> 1] = pack2(p0, p1);
+        if (rr & 2) ls1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[rr >> 1]), one2, ls1, false);
+        else        ls0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[rr >> 1]), one2, ls0, false);
+      }
+      ls = ls0 + ls1;
+    };
+    probs();
+    if (__any(!(ls <= kSumLimit))) {   // the max grew (or first chunk): rescale, redo
+      float mx = sc[0];
+#pragma unroll
+      for (int rr = 1; rr < 16; ++rr) mx = fmaxf(mx, sc[rr]);
+      mx = swap_max(mx) * c2;
+      if (mx > m_run) {
+        const float alpha = __builtin_amdgcn_exp2f(m_run - mx);
+        m_run = mx;
+        l_run *= alpha;
+        oacc[0] *= alpha;
+        oacc[1] *= alpha;
+      }
+      probs();
+    }
+    l_run += ls;
+    // O^T[db] += V^T . P^T over 2 key steps of 16 (V^T operands: keys
+    // 16 ks + 8 (e / 4) + 4 hw + e % 4, channel 32 db + lane % 32).
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const bf16x8 pb = __builtin_bit_cast(bf16x8, make_uint4(pk[4 * ks], pk[4 * ks + 1], pk[4 * ks + 2], pk[4 * ks + 3]));
 #pragma unroll
       for (int db = 0; db < 2; ++db) {
         const s16x4 x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vt + voff[db] + 2048 * ks));
@@ -356,74 +349,61 @@ k_attn_w64(AttnArgs a) {
   };
 
   const int n = p.n_chunks;
-  floatx16 sA[2], sB[2];   // scores of chunk c and c + 1, alternating roles
-  Chunk ch1;            // addresses of chunk c + 1 (its V is copied in iteration c)
-  int lo_c = 0, hi_c = 0, lo_n = 0, hi_n = 0;   // masks of chunks c and c + 1
+  int lo_c = 0, hi_c = 0;
   if (n > 0) {
     const Chunk ch0 = chunk_of(0);
-    copy_k(ch0, kA);
-    copy_v(ch0, vA);
+    copy(rk, ch0, kA, true);
+    copy(rv, ch0, vA, false);
     lo_c = ch0.lo;
     hi_c = ch0.hi;
-    if (n > 1) {
-      ch1 = chunk_of(1);
-      copy_k(ch1, kB);
-      lo_n = ch1.lo;
-      hi_n = ch1.hi;
-    }
   }
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   __syncthreads();
-  if (n > 0) scores(kA, sA);
-  // Both waves' reads of K(0) are done before K(2) is copied over it.
-  __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-  __syncthreads();
 
-  // Iteration c: scores of chunk c in sc, K(c + 1) in kr, V(c) in vr; the
-  // scores of chunk c + 1 go to sn.  K(c + 2) is copied into kw (where K(c)
-  // was) and V(c + 1) into vw (where V(c - 1) was).
-  auto body = [&](int c, floatx16 (&sc)[2], floatx16 (&sn)[2], const char* kr, const char* vr,
-                  char* kw, char* vw) {
-    if (c + 2 < n) {
-      const Chunk ch2 = chunk_of(c + 2);
-      copy_k(ch2, kw);
-      copy_v(ch1, vw);
-      ch1 = ch2;
-    } else {
-      copy_v(ch1, vw);
+  // Chunk c from buffers (kt, vt) while chunk c + 1 is copied into (kn, vn).
+  auto body = [&](int c, const char* kt, const char* vt, char* kn, char* vn) {
+    const int lo = lo_c, hi = hi_c;
+    if (c + 1 < n) {
+      const Chunk cn = chunk_of(c + 1);
+      copy(rk, cn, kn, true);
+      copy(rv, cn, vn, false);
+      lo_c = cn.lo;
+      hi_c = cn.hi;
     }
-    if (lo_c > 0 || hi_c < KC) mask(sc, lo_c, hi_c);
-    update_max(sc);
-    scores(kr, sn);
-    probs_pv(sc, vr);
-    lo_c = lo_n;
-    hi_c = hi_n;
-    lo_n = ch1.lo;
-    hi_n = ch1.hi;
-    // Copies issued above have landed (this wave's half) and both waves are
-    // past their reads of kr and vr before either copies into them.
+    step(kt, vt, lo, hi);
+    // Chunk c + 1 has landed (this wave's part) and every wave is past its
+    // reads of chunk c before any starts chunk c + 2 into the same buffers.
     __builtin_amdgcn_s_waitcnt(kWaitVm0);
     __syncthreads();
   };
-  // body(c) runs only while chunk c + 1 exists; the last chunk is finished
-  // without next scores or copies.
-  int c = 0;
-  for (; c + 2 < n; c += 2) {
-    body(c, sA, sB, kB, vA, kA, vB);
-    body(c + 1, sB, sA, kA, vB, kB, vA);
+  for (int c = 0; c < n; c += 2) {
+    body(c, kA, vA, kB, vB);
+    if (c + 1 < n) body(c + 1, kB, vB, kA, vA);
   }
-  if (c + 1 < n) {
-    body(c, sA, sB, kB, vA, kA, vB);
-    ++c;
+
+  // Merge the two key streams: stream 1 leaves (m, l, O) in LDS, stream 0
+  // combines and stores.  The K/V buffers are free after the last barrier.
+  float* xo = reinterpret_cast<float*>(qh ? kB : kA);   // [32 values][64 lanes]
+  float* xml = reinterpret_cast<float*>(vA) + 128 * qh; // [2][64 lanes]
+  if (sk == 1) {
+#pragma unroll
+    for (int db = 0; db < 2; ++db)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) xo[(16 * db + j) * 64 + lane] = oacc[db][j];
+    xml[lane] = m_run;
+    xml[64 + lane] = l_run;
   }
-  auto last = [&](floatx16 (&sc)[2], const char* vr) {
-    if (lo_c > 0 || hi_c < KC) mask(sc, lo_c, hi_c);
-    update_max(sc);
-    probs_pv(sc, vr);
-  };
-  if (c < n) {
-    if (c & 1) last(sB, vB);
-    else last(sA, vA);
+  __syncthreads();
+  if (sk == 1) return;
+  {
+    const float m1 = xml[lane], l1 = xml[64 + lane];
+    const float mm = fmaxf(m_run, m1);
+    const float a0 = __builtin_amdgcn_exp2f(m_run - mm), a1 = __builtin_amdgcn_exp2f(m1 - mm);
+    l_run = l_run * a0 + l1 * a1;
+#pragma unroll
+    for (int db = 0; db < 2; ++db)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) oacc[db][j] = oacc[db][j] * a0 + xo[(16 * db + j) * 64 + lane] * a1;
   }
 
   // Epilogue: O = O^T / l, 4 consecutive channels per store.
@@ -467,9 +447,9 @@ hipError_t launch_attn_w64(const AttnArgs& a0, hipStream_t s) {
   const int64_t total = (int64_t)a.batch * a.heads * a.groups_per_bh;
   if (total <= 0) return hipSuccess;
   if (a.dense)
-    hipLaunchKernelGGL(k_attn_w64<true>, dim3((unsigned)total), dim3(128), 0, s, a);
+    hipLaunchKernelGGL(k_attn_w64<true>, dim3((unsigned)total), dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL(k_attn_w64<false>, dim3((unsigned)total), dim3(128), 0, s, a);
+    hipLaunchKernelGGL(k_attn_w64<false>, dim3((unsigned)total), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -91,13 +91,16 @@ __device__ __forceinline__ uint64_t rank_key(double s) {
 
 // One workgroup per query block (i, h, b); thread j computes S[i][j] (the
 // channel-ordered sum of rounded products) and its rank.  The `keep` blocks of
-// lowest rank are kept and written in ascending block order.
-__global__ void __launch_bounds__(1024) k_gate_topk(IndexArgs a) {
+// lowest rank are kept and written in ascending block order.  The whole
+// pooled-k column of block j is requested before the first product, so the
+// gate costs one memory round trip.
+template <int D, int MAXT>
+__global__ void __launch_bounds__(MAXT) k_gate_topk(IndexArgs a) {
   extern __shared__ uint64_t keys[];   // [T_b]
   __shared__ int wave_kept[16];
   __shared__ int bad;
   const int i = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int D = a.head_dim, tb = a.n_tiles;
+  const int tb = a.n_tiles;
   const int j = threadIdx.x, lane = j & 63, wave = j >> 6;
   const int64_t bh = (int64_t)b * a.heads + h;
   if (j == 0) bad = 0;
@@ -106,13 +109,15 @@ __global__ void __launch_bounds__(1024) k_gate_topk(IndexArgs a) {
   if (j < tb) {
     const double* qr = a.qb + (bh * tb + i) * D;   // the same row for every thread
     const double* kc = a.kb + bh * D * tb + j;     // channel c of block j at kc[c * tb]
+    constexpr int BATCH = D < 64 ? D : 64;
     double s = 0.0;
-    for (int c0 = 0; c0 < D; c0 += 32) {
-      double kv[32];
 #pragma unroll
-      for (int u = 0; u < 32; ++u) kv[u] = kc[(int64_t)(c0 + u) * tb];
+    for (int c0 = 0; c0 < D; c0 += BATCH) {
+      double kv[BATCH];
 #pragma unroll
-      for (int u = 0; u < 32; ++u) {
+      for (int u = 0; u < BATCH; ++u) kv[u] = kc[(int64_t)(c0 + u) * tb];
+#pragma unroll
+      for (int u = 0; u < BATCH; ++u) {
         const double p = __dmul_rn(qr[c0 + u], kv[u]);
         s = (c0 + u == 0) ? p : __dadd_rn(s, p);
       }
@@ -207,7 +212,17 @@ hipError_t launch_pool(const IndexArgs& a, int dtype, hipStream_t s) {
 hipError_t launch_gate_topk(const IndexArgs& a, hipStream_t s) {
   dim3 grid(a.n_tiles, a.heads, a.batch), block(round_threads(a.n_tiles));
   size_t lds = sizeof(uint64_t) * (size_t)a.n_tiles;
-  hipLaunchKernelGGL(k_gate_topk, grid, block, lds, s, a);
+  // Small block counts get a small thread bound, which leaves registers to
+  // hold every pooled-k load of a thread in flight at once.
+  if (a.head_dim == 64) {
+    if (block.x <= 64) hipLaunchKernelGGL((k_gate_topk<64, 64>), grid, block, lds, s, a);
+    else if (block.x <= 256) hipLaunchKernelGGL((k_gate_topk<64, 256>), grid, block, lds, s, a);
+    else hipLaunchKernelGGL((k_gate_topk<64, 1024>), grid, block, lds, s, a);
+  } else {
+    if (block.x <= 64) hipLaunchKernelGGL((k_gate_topk<128, 64>), grid, block, lds, s, a);
+    else if (block.x <= 256) hipLaunchKernelGGL((k_gate_topk<128, 256>), grid, block, lds, s, a);
+    else hipLaunchKernelGGL((k_gate_topk<128, 1024>), grid, block, lds, s, a);
+  }
   return hipGetLastError();
 }
 

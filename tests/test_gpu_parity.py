@@ -212,3 +212,41 @@ def test_attention_convenience_call():
     assert img.shape == (1, 2, 4096, 64)
     _, full = run_gpu(w, qg, kg, vg)
     assert torch.equal(img, full[:, :, 256:])
+
+
+def test_graph_replay_matches_eager():
+    """A step (gate + attention) captured in a HIP graph and replayed several
+    times, with eager work on other inputs in between, equals the eager step
+    bit for bit on every replay."""
+    from paper_2605_15684_amd import ssba
+    w = preset("grid64_text", batch=1, heads=4)
+    (_, _, _), (qg, kg, vg) = inputs(w)
+    desc = gpu_desc(w, qg)
+    index, scratch = ssba.alloc_workspace(desc, qg.device)
+    out = torch.empty_like(qg)
+
+    def step():
+        ssba.build_index(qg, kg, desc, index, scratch)
+        ssba.forward(qg, kg, vg, index, desc, out)
+
+    step()
+    torch.cuda.synchronize()
+    ref_index, ref_out = index.clone(), out.clone()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    other = torch.randn_like(qg)
+    for rep in range(4):
+        index.fill_(-7)
+        out.zero_()
+        _, eager_other = run_gpu(w, other, kg, vg)     # unrelated eager work in between
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(index, ref_index), rep
+        assert torch.equal(out, ref_out), rep
+        assert eager_other.shape == out.shape
