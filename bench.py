@@ -45,11 +45,16 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 COPY_BYTES = 256 << 20
 
-# HBM traffic per launch from counter runs: kernel -> sources it was built
-# from (sha256 over their bytes, in order), FETCH_SIZE and WRITE_SIZE in KiB
-# per dispatch, and the copy calibration factors (bytes known / bytes read by
-# the counter).  Filled from the counter summaries kept with the profiles.
-MEASURED_TRAFFIC = {}
+# HBM traffic per launch from counter runs, keyed by kernel and workload:
+# the sources the kernel was built from (sha256 over their bytes, in order),
+# FETCH_SIZE and WRITE_SIZE in KiB per dispatch, and the copy calibration
+# factors (bytes known / bytes the counter reads for a plain 256 MiB copy).
+# From the counter summary in profiles/k_attn_w64_grid64.md.
+MEASURED_TRAFFIC = {
+    ("k_attn_w64<false>", "grid64"): {"sha": "98c58b6f661dcf03", "fetch_kib": 12495.1,
+                                      "write_kib": 8192.0, "fetch_factor": 1.9998,
+                                      "write_factor": 1.0},
+}
 
 
 def kernel_sources(kernel: str):
@@ -69,9 +74,9 @@ def sources_sha(kernel: str) -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel: str):
+def measured_traffic(kernel: str, workload: str):
     """HBM bytes per launch, or None if not measured on these sources."""
-    m = MEASURED_TRAFFIC.get(kernel)
+    m = MEASURED_TRAFFIC.get((kernel, workload))
     if not m or m["sha"] != sources_sha(kernel):
         return None
     return m["fetch_kib"] * 1024 * m["fetch_factor"] + m["write_kib"] * 1024 * m["write_factor"]
@@ -275,7 +280,7 @@ def main():
     achieved = f / (m["ms_fwd"] * 1e-3) / 1e12
     from paper_2605_15684_amd import _lib
     kernel = _lib.forward_kernel(r.desc)
-    traffic = measured_traffic(kernel)
+    traffic = measured_traffic(kernel, w.name)
     roofline = {"bound": "mfma", "kernel": kernel, "achieved": round(achieved, 2),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                 "traffic": None if traffic is None else round(traffic),
