@@ -17,6 +17,27 @@
 namespace ssba {
 namespace {
 
+// (block, head, batch) of a workgroup in a 1-D grid of n_tiles * heads *
+// batch workgroups.  Consecutive hardware ids go round-robin over the 8 XCDs;
+// when the (batch, head) count divides by 8, each XCD gets whole heads -- the
+// same heads the attention kernel gives it -- so pooled sums, index rows and
+// the head's Q/K stay in one XCD's L2 from kernel to kernel.
+__device__ __forceinline__ void unit_of(const IndexArgs& a, int& t, int& h, int& b) {
+  const int id = blockIdx.x, nbh = a.batch * a.heads;
+  int bh, r;
+  if ((nbh & 7) == 0) {
+    const int xcd = id & 7, s = id >> 3;
+    bh = xcd * (nbh >> 3) + s / a.n_tiles;
+    r = s % a.n_tiles;
+  } else {
+    bh = id / a.n_tiles;
+    r = id % a.n_tiles;
+  }
+  t = r;
+  b = bh / a.heads;
+  h = bh - b * a.heads;
+}
+
 // Block pooling.  One workgroup pools Q and K of one block.  The block's rows
 // are staged in LDS, up to 64 slots at a time, by all 256 threads with wide
 // loads; then 2 * D threads (one per channel of Q and of K) add the staged
@@ -34,7 +55,8 @@ __global__ void __launch_bounds__(256) k_pool(IndexArgs a) {
   constexpr int LOADS = 2 * SB * VPR;                  // per stage, Q then K
   using Vec = typename std::conditional<BF16, uint4, float>::type;
   __shared__ Vec stage[LOADS];
-  const int t = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  int t, h, b;
+  unit_of(a, t, h, b);
   const int tid = threadIdx.x;
   const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
   const int which = tid / D, c = tid % D;              // summing threads: tid < 2D
@@ -58,13 +80,19 @@ __global__ void __launch_bounds__(256) k_pool(IndexArgs a) {
     if (tid < 2 * D) {
       const char* col = reinterpret_cast<const char*>(stage) +
                         ((size_t)which * SB * D + c) * (BF16 ? 2 : 4);
-#pragma unroll 8
+      // Every staged value of the chain is read before the first add, so
+      // the dependent fp64 adds never wait on LDS.
+      float xs[SB];
+#pragma unroll
       for (int u = 0; u < SB; ++u) {
-        double x;
-        if (BF16)   // bf16 -> f32 -> f64 is exact
-          x = (double)__uint_as_float((uint32_t)*reinterpret_cast<const uint16_t*>(col + (size_t)u * D * 2) << 16);
+        if (BF16)   // bf16 -> f32 is exact
+          xs[u] = __uint_as_float((uint32_t)*reinterpret_cast<const uint16_t*>(col + (size_t)u * D * 2) << 16);
         else
-          x = (double)*reinterpret_cast<const float*>(col + (size_t)u * D * 4);
+          xs[u] = *reinterpret_cast<const float*>(col + (size_t)u * D * 4);
+      }
+#pragma unroll
+      for (int u = 0; u < SB; ++u) {
+        const double x = (double)xs[u];
         sum = (s0 + u == 0) ? x : __dadd_rn(sum, x);
       }
     }
@@ -99,7 +127,8 @@ __global__ void __launch_bounds__(MAXT) k_gate_topk(IndexArgs a) {
   extern __shared__ uint64_t keys[];   // [T_b]
   __shared__ int wave_kept[16];
   __shared__ int bad;
-  const int i = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  int i, h, b;
+  unit_of(a, i, h, b);
   const int tb = a.n_tiles;
   const int j = threadIdx.x, lane = j & 63, wave = j >> 6;
   const int64_t bh = (int64_t)b * a.heads + h;
@@ -128,7 +157,23 @@ __global__ void __launch_bounds__(MAXT) k_gate_topk(IndexArgs a) {
   }
   __syncthreads();
   bool kept = false;
-  if (j < tb) {
+  if (MAXT == 64) {
+    // One wave holds every key.  Radix select: T is the largest value with
+    // at least `keep` keys >= T (the keep-th largest key), found bit by bit
+    // from the top with wave ballots; keys above T are kept, and of the keys
+    // equal to T the lowest block ids fill the remaining places.
+    const bool valid = j < tb;
+    uint64_t thr = 0;
+#pragma unroll 8
+    for (int bit = 63; bit >= 0; --bit) {
+      const uint64_t cand = thr | (1ull << bit);
+      if (__popcll(__ballot(valid && key >= cand)) >= a.keep) thr = cand;
+    }
+    const bool gt = valid && key > thr, eq = valid && key == thr;
+    const int need = a.keep - __popcll(__ballot(gt));
+    const int before = __popcll(__ballot(eq) & ((1ull << lane) - 1ull));
+    kept = gt || (eq && before < need);
+  } else if (j < tb) {
     int rank = 0;
     for (int jj = 0; jj < tb; ++jj) {
       const uint64_t kj = keys[jj];
@@ -155,7 +200,8 @@ __global__ void __launch_bounds__(MAXT) k_gate_topk(IndexArgs a) {
 
 // Window (win_h x win_w blocks of the shifted frame) and dense gates.
 __global__ void __launch_bounds__(1024) k_gate_static(IndexArgs a, int gate) {
-  const int i = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  int i, h, b;
+  unit_of(a, i, h, b);
   const int tb = a.n_tiles, nx = a.f.nx;
   const int j = threadIdx.x;
   const int64_t bh = (int64_t)b * a.heads + h;
@@ -185,7 +231,7 @@ int round_threads(int n) { return ((n + 63) / 64) * 64; }
 
 template <int DTYPE, int D>
 void launch_pool_d(const IndexArgs& a, hipStream_t s) {
-  dim3 grid(a.n_tiles, a.heads, a.batch), block(256);
+  dim3 grid(a.n_tiles * a.heads * a.batch), block(256);
   switch (a.f.tile_log2) {
     case 2: hipLaunchKernelGGL((k_pool<DTYPE, 2, D>), grid, block, 0, s, a); break;
     case 3: hipLaunchKernelGGL((k_pool<DTYPE, 3, D>), grid, block, 0, s, a); break;
@@ -210,7 +256,7 @@ hipError_t launch_pool(const IndexArgs& a, int dtype, hipStream_t s) {
 }
 
 hipError_t launch_gate_topk(const IndexArgs& a, hipStream_t s) {
-  dim3 grid(a.n_tiles, a.heads, a.batch), block(round_threads(a.n_tiles));
+  dim3 grid(a.n_tiles * a.heads * a.batch), block(round_threads(a.n_tiles));
   size_t lds = sizeof(uint64_t) * (size_t)a.n_tiles;
   // Small block counts get a small thread bound, which leaves registers to
   // hold every pooled-k load of a thread in flight at once.
@@ -227,7 +273,7 @@ hipError_t launch_gate_topk(const IndexArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_gate_static(const IndexArgs& a, int gate, hipStream_t s) {
-  dim3 grid(a.n_tiles, a.heads, a.batch), block(round_threads(a.n_tiles));
+  dim3 grid(a.n_tiles * a.heads * a.batch), block(round_threads(a.n_tiles));
   hipLaunchKernelGGL(k_gate_static, grid, block, 0, s, a, gate);
   return hipGetLastError();
 }
