@@ -49,17 +49,13 @@ COPY_BYTES = 256 << 20
 # the sources the kernel was built from (sha256 over their bytes, in order),
 # FETCH_SIZE and WRITE_SIZE in KiB per dispatch, and the copy calibration
 # factors (bytes known / bytes the counter reads for a plain 256 MiB copy).
-# From the counter summary in profiles/k_attn_w64_grid64.md.
-MEASURED_TRAFFIC = {
-    ("k_attn_w64<false>", "grid64"): {"sha": "98c58b6f661dcf03", "fetch_kib": 12495.1,
-                                      "write_kib": 8192.0, "fetch_factor": 1.9998,
-                                      "write_factor": 1.0},
-}
+# From the counter summary in profiles/k_attn_mfma_grid64.md.
+MEASURED_TRAFFIC = {}
 
 
 def kernel_sources(kernel: str):
     base = os.path.join(ROOT, "paper_2605_15684_amd", "csrc")
-    own = {"k_attn_w64": "ssba_attn_w64.hip", "k_attn_bf16": "ssba_attn_bf16.hip",
+    own = {"k_attn_mfma": "ssba_attn_mfma.hip", "k_attn_bf16": "ssba_attn_bf16.hip",
            "k_attn_f32": "ssba_attn_f32.hip"}[kernel.split("<")[0]]
     return [os.path.join(base, own), os.path.join(base, "ssba_common.h"),
             os.path.join(ROOT, "include", "ssba.h")]

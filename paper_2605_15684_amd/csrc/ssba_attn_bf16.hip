@@ -387,8 +387,8 @@ hipError_t launch_t(const AttnArgs& a0, hipStream_t s) {
 
 const char* attn_kernel_name(const AttnArgs& a, int head_dim, int tile, int dtype) {
   if (dtype == SSBA_DT_F32) return head_dim == 64 ? "k_attn_f32<64>" : "k_attn_f32<128>";
-  if (w64_supported(head_dim, tile, a.dense != 0, a.n_tiles, a.seq, (int64_t)a.seq * a.st))
-    return w64_kernel_name(a.dense != 0);
+  if (mfma_supported(head_dim, tile, a.dense != 0, a.n_tiles, a.seq, (int64_t)a.seq * a.st))
+    return mfma_kernel_name(head_dim, tile, a.dense != 0);
   static const char* const names[2][3] = {
       {"k_attn_bf16<64, 2>", "k_attn_bf16<64, 3>", "k_attn_bf16<64, 4>"},
       {"k_attn_bf16<128, 2>", "k_attn_bf16<128, 3>", "k_attn_bf16<128, 4>"}};
@@ -396,8 +396,8 @@ const char* attn_kernel_name(const AttnArgs& a, int head_dim, int tile, int dtyp
 }
 
 hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, int tile, hipStream_t s) {
-  if (w64_supported(head_dim, tile, a.dense != 0, a.n_tiles, a.seq, (int64_t)a.seq * a.st))
-    return launch_attn_w64(a, s);
+  if (mfma_supported(head_dim, tile, a.dense != 0, a.n_tiles, a.seq, (int64_t)a.seq * a.st))
+    return launch_attn_mfma(a, head_dim, tile, s);
   if (head_dim == 64) {
     if (tile == 4) return launch_t<64, 2>(a, s);
     if (tile == 8) return launch_t<64, 3>(a, s);

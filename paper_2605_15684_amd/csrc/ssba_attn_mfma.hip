@@ -1,23 +1,24 @@
-// SSBA attention forward, bf16, head_dim 64, 64 query rows per workgroup.
+// SSBA attention forward, bf16, head_dim 64 or 128, 8x8- or 16x16-token
+// blocks: 64 query rows per workgroup.
 //
-// Specialised path for the 1024-px class shapes (8x8-token blocks, so one
-// query block is exactly 64 rows) and for natural-order rows (text queries,
-// dense control).  Computes the attend step of Algorithm 1 like the generic
-// kernel; it differs only in how data reaches the matrix cores.
+// Computes the attend step of Algorithm 1 (image queries of a block attend to
+// the image keys of its kept blocks and to every text key; text queries, and
+// every query in the dense control, attend to every key in natural order)
+// like the generic kernel; it differs only in how data reaches the matrix
+// cores.
 //
 // At head_dim 64 the softmax of a block pair costs as many VALU cycles as its
-// two products cost MFMA cycles, so the kernel is built for overlap between
-// waves:
-//   * a workgroup owns the 64 query rows of one block with four waves: wave w
-//     takes queries 32 (w % 2) .. + 31 and the keys 32 (w / 2) .. + 31 of every
-//     64-key chunk (one 8x4 half of a kept block), so each SIMD holds four
-//     waves; the two key streams are merged once at the end;
+// two products cost MFMA cycles; at 128 the products dominate.  The kernel:
+//   * four waves own 64 query rows (one 8x8 block, or a quarter of a 16x16
+//     block): wave w takes queries 32 (w % 2) .. + 31 and the keys
+//     32 (w / 2) .. + 31 of every 64-key chunk; the two key streams are merged
+//     once at the end;
 //   * every 32-key half chunk of K and V is copied once per workgroup, by DMA
 //     (buffer_load_dwordx4 ... lds; the two waves of a stream split it), into
 //     double-buffered LDS.  Row offsets are scalar operands and the per-lane
-//     part is one VGPR per chunk, so a copy costs almost no vector ALU work.
-//     Out-of-range rows read as zeros (the buffer bound is the (batch, head)
-//     slice);
+//     part is one VGPR per copy instruction and chunk, so a copy costs almost
+//     no vector ALU work.  Out-of-range rows read as zeros (the buffer bound
+//     is the (batch, head) slice);
 //   * the softmax is optimistic: probabilities are taken against the running
 //     max; only when a lane's chunk sum exceeds 2^20 (the max grew, or the
 //     first chunk) is the chunk max taken, O and l rescaled and the chunk
@@ -33,15 +34,19 @@
 //   A[i][k]: lane holds row i = l % 32, k = 8 hw + e  (e = 0..7)
 //   B[k][j]: lane holds col j = l % 32, k = 8 hw + e
 //   D[i][j]: lane holds col j = l % 32, rows i = 8 (r / 4) + 4 hw + r % 4 (r = 0..15)
-// In S^T the lane holds, for its query, the keys 32 kb + 8 (r / 4) + 4 hw + r % 4.
-// The 16-key step ks of P V contracts keys 16 ks + 8 (e / 4) + 4 hw + e % 4
-// for element e: exactly the lane's own probabilities, so P^T never leaves
-// its registers.
+// In S^T the lane holds, for its query, the keys 8 (r / 4) + 4 hw + r % 4 of
+// the half chunk.  The 16-key step ks of P V contracts keys
+// 16 ks + 8 (e / 4) + 4 hw + e % 4 for element e: exactly the lane's own
+// probabilities, so P^T never leaves its registers.
 //
-// LDS tiles are 32 rows (keys) of 128 bytes.  A 16-byte column chunk c of key
-// k sits at chunk c ^ ((k >> 1) & 7) in the K tile and c ^ (4 ((k >> 1) & 1))
-// in the V tile; with these swizzles the K operand reads (ds_read_b128), the
-// V transposing reads and the DMA writes all spread evenly over the banks.
+// LDS tiles hold 32 keys of 2 D bytes; 16-byte column chunks are permuted
+// per key so that the DMA writes, the K operand reads (ds_read_b128, 16
+// consecutive keys at one logical chunk) and the V transposing reads (4 keys
+// x 64 bytes per half wave) spread evenly over the 64 banks:
+//   K, D 64:  chunk c of key k at c ^ ((k >> 1) & 7)   (two keys per 256 B)
+//   K, D 128: chunk c of key k at c ^ (k & 15)
+//   V, D 64:  chunk c of key k at c ^ (4 ((k >> 1) & 1))
+//   V, D 128: chunk c of key k at c ^ (4 (k & 3))
 #include <hip/hip_runtime.h>
 #include <hip/hip_bf16.h>
 
@@ -60,33 +65,48 @@ typedef uint16_t u16;
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 typedef __attribute__((address_space(3))) void lds_void;
 
-constexpr int D = 64;
-constexpr int KC = 64;                 // keys per chunk (one 8x8 block)
+constexpr int KC = 64;                 // keys per chunk
 constexpr int KH = 32;                 // keys per stream and chunk
-constexpr int HALF_BYTES = KH * D * 2; // one K or V half chunk in LDS (4 KB)
 constexpr float kSumLimit = 1048576.0f;   // 2^20: redo a chunk above this lane sum
-// s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt
+// s_waitcnt immediate (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt
 // 6:4, lgkmcnt 11:8): every vector memory operation done.
 constexpr int kWaitVm0 = 0x0F70;
 // Buffer resource word 3 for raw (unformatted, unswizzled) dword access.
 constexpr int kRawBufferFlags = 0x00020000;
 
+template <int D, int TILE_LOG2>
+struct Shape {
+  static constexpr int BT = 1 << TILE_LOG2;        // block side (tokens)
+  static constexpr int CPR = D / 8;                // 16-byte chunks per key row
+  static constexpr int ROWB = 2 * D;               // bytes per key row
+  static constexpr int KPI = 1024 / ROWB;          // keys per copy instruction
+  static constexpr int NI = KH / KPI;              // copy instructions per half chunk
+  static constexpr int NIW = NI / 2;               // ... per wave
+  static constexpr int HALF = KH * ROWB;           // bytes of a half chunk tile
+  static constexpr int CPB = BT * BT / KC;         // chunks per kept block
+  static constexpr int GPB = BT * BT / 64;         // 64-query groups per block
+  static constexpr int NKS = D / 16;               // 16-channel steps of Q K^T
+  static constexpr int NDB = D / 32;               // 32-channel tiles of O
+  static_assert(KPI <= BT, "a copy instruction stays inside one block row");
+  static_assert(NIW <= 4, "copy instructions per wave fit a Chunk");
+};
+
 // Where one workgroup's keys come from.
 struct Plan {
-  int img_chunks;    // leading chunks drawn from kept blocks (8x8 = 64 keys each)
+  int img_chunks;    // leading chunks drawn from kept blocks
   int n_chunks;      // total chunks
   int natural_end;   // > 0: keys are rows [0, natural_end) in order
 };
 
-// Copy addresses of this stream's half of one chunk: copy instruction m
-// (0..3; the wave issues two of them) lane l moves key 8 m + l / 8 of the
-// half from element row row0 + m * step (+ wrap when y0 + m < 0: a block row
-// above the grid wraps to its bottom) and byte lane_off within that row's
-// 8-key group, relative to the (batch, head) slice.  Keys outside [lo, hi)
-// of the half are masked.
+// Copy addresses of this stream's half of one chunk, for copy instruction
+// m = NIW * (wave % 2) + mm (NIW <= 4): element row row0 + rstep * ((KPI m) / BT)
+// (+ wrap when the block row lies above the grid) and per-lane byte offset
+// lane_off[mm] within that row, relative to the (batch, head) slice.  Keys
+// outside [lo, hi) of the half are masked.  (A plain struct: with a
+// per-shape template the host compiler drops the kernels' launch stubs.)
 struct Chunk {
-  int row0, step, y0;
-  unsigned lane_off;
+  int row0, rstep, y0;
+  unsigned lane_off[4];
   int lo, hi;
 };
 
@@ -105,17 +125,21 @@ __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
 }
 
 // DENSE: every group runs natural-order rows over all keys (no index).
-template <bool DENSE>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4)))
-k_attn_w64(AttnArgs a) {
+template <int D, int TILE_LOG2, bool DENSE>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 64 ? 4 : 2)))
+k_attn_mfma(AttnArgs a) {
+  using S = Shape<D, TILE_LOG2>;
+  constexpr int BT = S::BT, CPR = S::CPR, KPI = S::KPI, NIW = S::NIW, HALF = S::HALF;
+  constexpr int CPB = S::CPB, GPB = S::GPB, NKS = S::NKS, NDB = S::NDB;
+
   // K and V buffers A and B (alternate chunks); stream s uses bytes
-  // [4096 s, 4096 s + 4096) of each.  Declared separately so every access
+  // [HALF s, HALF (s + 1)) of each.  Declared separately so every access
   // names one buffer statically: the compiler can then tell that a read of
   // one chunk does not overlap the copy of the next still in flight.
-  __shared__ __attribute__((aligned(16))) char kA[2 * HALF_BYTES];
-  __shared__ __attribute__((aligned(16))) char kB[2 * HALF_BYTES];
-  __shared__ __attribute__((aligned(16))) char vA[2 * HALF_BYTES];
-  __shared__ __attribute__((aligned(16))) char vB[2 * HALF_BYTES];
+  __shared__ __attribute__((aligned(16))) char kA[2 * HALF];
+  __shared__ __attribute__((aligned(16))) char kB[2 * HALF];
+  __shared__ __attribute__((aligned(16))) char vA[2 * HALF];
+  __shared__ __attribute__((aligned(16))) char vB[2 * HALF];
 
   // Logical group id.  Consecutive hardware ids go round-robin over the 8
   // XCDs; when the (batch, head) count divides by 8 each XCD gets whole
@@ -166,21 +190,22 @@ k_attn_w64(AttnArgs a) {
     p.natural_end = a.seq;
     p.n_chunks = (a.seq + KC - 1) / KC;
   } else {
-    const int i = r - a.n_text_groups;
-    qrow = frame_row(a.f, i, 32 * qh + l32);
+    const int g = r - a.n_text_groups;     // image group: block i, quarter gq
+    const int i = g / GPB, gq = g - i * GPB;
+    qrow = frame_row(a.f, i, 64 * gq + 32 * qh + l32);
     const int32_t* list = a.index + (bh * (int64_t)a.n_tiles + i) * (a.n_tiles + 1);
     const int count = min(max(list[0], 0), min(a.n_tiles, 64));
     const int e = lane < count ? list[1 + lane] : 0;
     listv = (unsigned)e < (unsigned)a.n_tiles ? e : -1;
-    p.img_chunks = count;
+    p.img_chunks = CPB * count;
     p.natural_end = 0;
     p.n_chunks = p.img_chunks + (a.f.n_text + KC - 1) / KC;
   }
 
   // Q^T operand [ks]: query 32 qh + l32, channels 16 ks + 8 hw + [0, 8).
-  bf16x8 qf[4];
+  bf16x8 qf[NKS];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks)
+  for (int ks = 0; ks < NKS; ++ks)
     qf[ks] = *reinterpret_cast<const bf16x8*>(qbase + max(qrow, 0) * st + 16 * ks + 8 * hw);
 
   // Buffer resources over this (batch, head) slice: rows [0, seq).
@@ -190,53 +215,73 @@ k_attn_w64(AttnArgs a) {
   const __amdgpu_buffer_rsrc_t rv =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<u16*>(vbase), (short)0, (int)slice_bytes, kRawBufferFlags);
 
-  // DMA lane mapping: lane l of instruction m fills key 8 m + l / 8 of the
-  // half, physical chunk l % 8 -- logical K chunk (l % 8) ^ ((key >> 1) & 7)
-  // and logical V chunk (l % 8) ^ (4 ((key >> 1) & 1)), where
-  // (key >> 1) & 7 = 4 (m & 1) + l / 16.
-  const int vk = lane >> 3;
-  const unsigned kc0 = 16u * ((lane & 7) ^ (lane >> 4));          // bytes, m even
-  const unsigned kc1 = 16u * ((lane & 7) ^ (4 + (lane >> 4)));    // bytes, m odd
-  const unsigned vcb = 16u * ((lane & 7) ^ (4 * ((lane >> 4) & 1)));
+  // DMA lane mapping: lane l of copy instruction m fills key KPI m + l / CPR
+  // of the half, physical chunk l % CPR; it fetches the logical chunk that
+  // the swizzle puts there.  kcol[mm] / vcol: that chunk's byte offset.
+  const int kin = lane / CPR, pch = lane % CPR;   // key within the instruction, physical chunk
+  unsigned kcol[NIW], vcol;
+#pragma unroll
+  for (int mm = 0; mm < NIW; ++mm) {
+    const int key = KPI * (NIW * qh + mm) + kin;
+    const int lc = D == 64 ? (pch ^ ((key >> 1) & 7)) : (pch ^ (key & 15));
+    kcol[mm] = 16u * lc;
+  }
+  {
+    const int key = kin;   // the V swizzle depends on key bits that KPI m leaves unchanged
+    const int lc = D == 64 ? (pch ^ (4 * ((key >> 1) & 1))) : (pch ^ (4 * (key & 3)));
+    vcol = 16u * lc;
+  }
   // K operand reads: key l32, logical chunk 2 ks + hw.
-  const int g = (l32 >> 1) & 7;
-  int koff[4];
+  int koff[NKS];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) koff[ks] = HALF_BYTES * sk + l32 * 128 + 16 * ((2 * ks + hw) ^ g);
-  // V transposing reads: 16-lane group G = lane / 16, i = lane % 16 points at
-  // key 16 ks + 8 r' + 4 hw + i / 4, channels 32 db + 16 (G % 2) + 4 (i % 4).
+  for (int ks = 0; ks < NKS; ++ks) {
+    const int lc = 2 * ks + hw;
+    const int pc = D == 64 ? (lc ^ ((l32 >> 1) & 7)) : (lc ^ (l32 & 15));
+    koff[ks] = HALF * sk + l32 * S::ROWB + 16 * pc;
+  }
+  // V transposing reads: 16-lane group G = lane / 16, i = lane % 16 reads
+  // key 16 ks + 8 r' + 4 hw + i / 4 (r' = 0, 1: the two reads of a step),
+  // channels 32 db + 16 (G % 2) + 4 (i % 4) .. + 3.
   const int G = lane >> 4, li = lane & 15;
-  int voff[2];
+  int voff[NDB];
 #pragma unroll
-  for (int db = 0; db < 2; ++db)
-    voff[db] = HALF_BYTES * sk + (4 * hw + (li >> 2)) * 128 + 64 * (db ^ ((li >> 3) & 1)) +
-               32 * (G & 1) + 8 * (li & 3);
+  for (int db = 0; db < NDB; ++db) {
+    const int key = 4 * hw + (li >> 2);                 // + 8 r' + 16 ks (swizzle-neutral)
+    const int lc = 4 * db + 2 * (G & 1) + ((li & 3) >> 1);
+    const int pc = D == 64 ? (lc ^ (4 * ((key >> 1) & 1))) : (lc ^ (4 * (key & 3)));
+    voff[db] = HALF * sk + key * S::ROWB + 16 * pc + 8 * (li & 1);
+  }
 
   // Frame origin (y0, x0) of each kept block, one block per lane.
   const int W = a.f.grid_w, H = a.f.grid_h;
   int orig_y = 0, orig_x = 0;
   if (listv >= 0) {
     const int ty = listv / a.f.nx;
-    orig_y = ty * 8 - a.f.sy;
-    orig_x = (listv - ty * a.f.nx) * 8 - a.f.sx;
+    orig_y = ty * BT - a.f.sy;
+    orig_x = (listv - ty * a.f.nx) * BT - a.f.sx;
   }
 
-  // This stream's half of chunk c.  Image chunks: block rows 4 sk .. 4 sk + 3;
-  // each lane's column wraps to the right edge when it starts left of it.
-  // Natural-order chunks always cover 64 existing rows: a ragged last chunk
-  // is moved back to end at the last row and masks the keys the previous
-  // chunk already covered (rows of a ragged text chunk that run into the
-  // image rows exist too).
+  // This stream's half of chunk c.  Image chunks: block list[c / CPB], block
+  // rows (c % CPB) * 64 / BT + sk * 32 / BT onwards; each lane's column wraps
+  // to the right edge when it starts left of it.  Natural-order chunks always
+  // cover 64 existing rows: a ragged last chunk is moved back to end at the
+  // last row and masks the keys the previous chunk already covered (rows of a
+  // ragged text chunk that run into the image rows exist too).
   auto chunk_of = [&](int c) {
     Chunk ch;
     if (!DENSE && c < p.img_chunks) {
-      const int j = __builtin_amdgcn_readlane(listv, c);
-      const int x0 = __builtin_amdgcn_readlane(orig_x, c);
-      ch.y0 = __builtin_amdgcn_readlane(orig_y, c) + 4 * sk;
+      const int e = c / CPB, sub = c - e * CPB;
+      const int j = __builtin_amdgcn_readlane(listv, e);
+      const int x0 = __builtin_amdgcn_readlane(orig_x, e);
+      ch.y0 = __builtin_amdgcn_readlane(orig_y, e) + sub * (KC / BT) + sk * (KH / BT);
       ch.row0 = a.f.n_text + ch.y0 * W;
-      ch.step = W;
-      const unsigned x = (unsigned)(x0 + vk);
-      ch.lane_off = 2u * min(x, x + (unsigned)W) * (unsigned)st;   // x < 0 wraps by W
+      ch.rstep = W;
+#pragma unroll
+      for (int mm = 0; mm < NIW; ++mm) {
+        const int col = (KPI * (NIW * qh + mm)) % BT + kin;
+        const unsigned x = (unsigned)(x0 + col);
+        ch.lane_off[mm] = 2u * min(x, x + (unsigned)W) * (unsigned)st;   // x < 0 wraps by W
+      }
       ch.lo = 0;
       ch.hi = j >= 0 ? KH : 0;
       return ch;
@@ -251,33 +296,40 @@ k_attn_w64(AttnArgs a) {
     }
     ch.lo = min(max(lo - KH * sk, 0), KH);
     ch.hi = min(max(hi - KH * sk, 0), KH);
+    // Natural rows: instruction m covers rows base + 32 sk + KPI m + [0, KPI).
     ch.row0 = base + KH * sk;
-    ch.step = 8;
+    ch.rstep = BT;   // (KPI m) / BT rows of BT keys: row0 + KPI m after the column term below
     ch.y0 = 0;
-    ch.lane_off = 2u * (unsigned)(vk * st);
+#pragma unroll
+    for (int mm = 0; mm < NIW; ++mm) {
+      const int col = (KPI * (NIW * qh + mm)) % BT + kin;
+      ch.lane_off[mm] = 2u * (unsigned)(col * st);
+    }
     return ch;
   };
   const int wrap = H * W;
 
-  // This wave's two of the four copy instructions of a half chunk, into
-  // the stream's 4 KB of buffer `dst`.  The LDS base is kept opaque so each
-  // instruction's LDS address is one scalar add rather than a held register.
+  // This wave's NIW of the NI copy instructions of a half chunk, into its
+  // stream's HALF bytes of buffer `dst`.  The LDS base is kept opaque so
+  // each instruction's LDS address is one scalar add rather than a held
+  // register.
   auto copy = [&](const __amdgpu_buffer_rsrc_t& rs, const Chunk& ch, char* dst, bool is_k) {
-    int lb = HALF_BYTES * sk + 2048 * qh;
+    int lb = HALF * sk + 1024 * NIW * qh;
     asm volatile("" : "+s"(lb));
 #pragma unroll
-    for (int mm = 0; mm < 2; ++mm) {
-      const int m = 2 * qh + mm;
-      const int row = ch.row0 + m * ch.step + (ch.y0 + m < 0 ? wrap : 0);
-      const unsigned col = is_k ? ((mm & 1) ? kc1 : kc0) : vcb;
+    for (int mm = 0; mm < NIW; ++mm) {
+      const int m = NIW * qh + mm;
+      const int rr = (KPI * m) / BT;   // block row of the instruction within the half
+      const int row = ch.row0 + rr * ch.rstep + (ch.y0 + rr < 0 ? wrap : 0);
+      const unsigned col = is_k ? kcol[mm] : vcol;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(dst + lb + 1024 * mm), 16,
-                                               ch.lane_off + col, 2u * (unsigned)row * (unsigned)st, 0, 0);
+                                               ch.lane_off[mm] + col, 2u * (unsigned)row * (unsigned)st, 0, 0);
     }
   };
 
-  floatx16 oacc[2];   // [db]
-  oacc[0] = floatx16{};
-  oacc[1] = floatx16{};
+  floatx16 oacc[NDB];   // [db]
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) oacc[db] = floatx16{};
   float m_run = -1e30f, l_run = 0.f;
   const float c2 = a.scale_log2;
   const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
@@ -288,7 +340,7 @@ k_attn_w64(AttnArgs a) {
     // S^T = K . Q^T: the lane's 16 keys 8 (r / 4) + 4 hw + r % 4 of its query.
     floatx16 sc = floatx16{};
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
+    for (int ks = 0; ks < NKS; ++ks) {
       const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kt + koff[ks]);
       sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sc, 0, 0, 0);
     }
@@ -327,8 +379,8 @@ k_attn_w64(AttnArgs a) {
         const float alpha = __builtin_amdgcn_exp2f(m_run - mx);
         m_run = mx;
         l_run *= alpha;
-        oacc[0] *= alpha;
-        oacc[1] *= alpha;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) oacc[db] *= alpha;
       }
       probs();
     }
@@ -339,9 +391,9 @@ k_attn_w64(AttnArgs a) {
     for (int ks = 0; ks < 2; ++ks) {
       const bf16x8 pb = __builtin_bit_cast(bf16x8, make_uint4(pk[4 * ks], pk[4 * ks + 1], pk[4 * ks + 2], pk[4 * ks + 3]));
 #pragma unroll
-      for (int db = 0; db < 2; ++db) {
-        const s16x4 x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vt + voff[db] + 2048 * ks));
-        const s16x4 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vt + voff[db] + 2048 * ks + 1024));
+      for (int db = 0; db < NDB; ++db) {
+        const s16x4 x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vt + voff[db] + 16 * S::ROWB * ks));
+        const s16x4 x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vt + voff[db] + 16 * S::ROWB * ks + 8 * S::ROWB));
         const s16x8 v8 = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, v8), pb, oacc[db], 0, 0, 0);
       }
@@ -383,11 +435,12 @@ k_attn_w64(AttnArgs a) {
 
   // Merge the two key streams: stream 1 leaves (m, l, O) in LDS, stream 0
   // combines and stores.  The K/V buffers are free after the last barrier.
-  float* xo = reinterpret_cast<float*>(qh ? kB : kA);   // [32 values][64 lanes]
+  static_assert(16 * NDB * 64 * 4 <= 2 * HALF, "merge area fits one buffer");
+  float* xo = reinterpret_cast<float*>(qh ? kB : kA);   // [16 NDB values][64 lanes]
   float* xml = reinterpret_cast<float*>(vA) + 128 * qh; // [2][64 lanes]
   if (sk == 1) {
 #pragma unroll
-    for (int db = 0; db < 2; ++db)
+    for (int db = 0; db < NDB; ++db)
 #pragma unroll
       for (int j = 0; j < 16; ++j) xo[(16 * db + j) * 64 + lane] = oacc[db][j];
     xml[lane] = m_run;
@@ -401,7 +454,7 @@ k_attn_w64(AttnArgs a) {
     const float a0 = __builtin_amdgcn_exp2f(m_run - mm), a1 = __builtin_amdgcn_exp2f(m1 - mm);
     l_run = l_run * a0 + l1 * a1;
 #pragma unroll
-    for (int db = 0; db < 2; ++db)
+    for (int db = 0; db < NDB; ++db)
 #pragma unroll
       for (int j = 0; j < 16; ++j) oacc[db][j] = oacc[db][j] * a0 + xo[(16 * db + j) * 64 + lane] * a1;
   }
@@ -412,7 +465,7 @@ k_attn_w64(AttnArgs a) {
   if (qrow >= 0) {
     u16* orow = obase + qrow * st;
 #pragma unroll
-    for (int db = 0; db < 2; ++db)
+    for (int db = 0; db < NDB; ++db)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const uint2 wv = make_uint2(pack2(oacc[db][4 * j] * inv, oacc[db][4 * j + 1] * inv),
@@ -424,32 +477,49 @@ k_attn_w64(AttnArgs a) {
 
 }  // namespace
 
-const char* w64_kernel_name(bool dense) { return dense ? "k_attn_w64<true>" : "k_attn_w64<false>"; }
-
-bool w64_supported(int head_dim, int tile, bool dense, int n_tiles, int seq, int64_t span) {
-  // 32-bit byte offsets inside one (batch, head); at most 64 kept blocks;
-  // natural-order chunks need at least one full chunk of rows.
-  return head_dim == 64 && (dense || (tile == 8 && n_tiles <= 64)) && seq >= KC &&
-         span < ((int64_t)1 << 31);
+const char* mfma_kernel_name(int head_dim, int tile, bool dense) {
+  static const char* const names[2][2][2] = {
+      {{"k_attn_mfma<64, 3, false>", "k_attn_mfma<64, 3, true>"},
+       {"k_attn_mfma<64, 4, false>", "k_attn_mfma<64, 4, true>"}},
+      {{"k_attn_mfma<128, 3, false>", "k_attn_mfma<128, 3, true>"},
+       {"k_attn_mfma<128, 4, false>", "k_attn_mfma<128, 4, true>"}}};
+  // The dense control runs natural-order rows only; it uses the 8x8 shape.
+  const int ti = (!dense && tile == 16) ? 1 : 0;
+  return names[head_dim == 64 ? 0 : 1][ti][dense ? 1 : 0];
 }
 
-hipError_t launch_attn_w64(const AttnArgs& a0, hipStream_t s) {
+bool mfma_supported(int head_dim, int tile, bool dense, int n_tiles, int seq, int64_t span) {
+  // 32-bit byte offsets inside one (batch, head); at most 64 kept blocks;
+  // natural-order chunks need at least one full chunk of rows.
+  return (head_dim == 64 || head_dim == 128) && (dense || ((tile == 8 || tile == 16) && n_tiles <= 64)) &&
+         seq >= KC && 2 * span < ((int64_t)1 << 32);
+}
+
+hipError_t launch_attn_mfma(const AttnArgs& a0, int head_dim, int tile, hipStream_t s) {
   AttnArgs a = a0;
+  const int gpb = (tile == 16) ? 4 : 1;   // 64-query groups per image block
   if (a.dense) {
     a.n_text_groups = (a.seq + 63) / 64;    // every group runs natural-order rows
     a.groups_per_tile = 1;
     a.groups_per_bh = a.n_text_groups;
   } else {
     a.n_text_groups = (a.f.n_text + 63) / 64;
-    a.groups_per_tile = 1;
-    a.groups_per_bh = a.n_text_groups + a.n_tiles;
+    a.groups_per_tile = gpb;
+    a.groups_per_bh = a.n_text_groups + a.n_tiles * gpb;
   }
   const int64_t total = (int64_t)a.batch * a.heads * a.groups_per_bh;
   if (total <= 0) return hipSuccess;
-  if (a.dense)
-    hipLaunchKernelGGL(k_attn_w64<true>, dim3((unsigned)total), dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL(k_attn_w64<false>, dim3((unsigned)total), dim3(256), 0, s, a);
+  const dim3 grid((unsigned)total), block(256);
+  const bool big = !a.dense && tile == 16;
+  if (head_dim == 64) {
+    if (a.dense) hipLaunchKernelGGL((k_attn_mfma<64, 3, true>), grid, block, 0, s, a);
+    else if (big) hipLaunchKernelGGL((k_attn_mfma<64, 4, false>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((k_attn_mfma<64, 3, false>), grid, block, 0, s, a);
+  } else {
+    if (a.dense) hipLaunchKernelGGL((k_attn_mfma<128, 3, true>), grid, block, 0, s, a);
+    else if (big) hipLaunchKernelGGL((k_attn_mfma<128, 4, false>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((k_attn_mfma<128, 3, false>), grid, block, 0, s, a);
+  }
   return hipGetLastError();
 }
 

@@ -69,9 +69,9 @@ hipError_t launch_gate_static(const IndexArgs& a, int gate, hipStream_t s);
 hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, int tile, hipStream_t s);
 hipError_t launch_attn_f32(const AttnArgs& a, int head_dim, int tile, hipStream_t s);
 // One-wave-per-64-rows bf16 kernel for head_dim 64 (8x8 blocks or dense).
-bool w64_supported(int head_dim, int tile, bool dense, int n_tiles, int seq, int64_t span);
-hipError_t launch_attn_w64(const AttnArgs& a, hipStream_t s);
-const char* w64_kernel_name(bool dense);
+bool mfma_supported(int head_dim, int tile, bool dense, int n_tiles, int seq, int64_t span);
+hipError_t launch_attn_mfma(const AttnArgs& a, int head_dim, int tile, hipStream_t s);
+const char* mfma_kernel_name(int head_dim, int tile, bool dense);
 // Name of the kernel launch_attn_bf16 / launch_attn_f32 would run.
 const char* attn_kernel_name(const AttnArgs& a, int head_dim, int tile, int dtype);
 

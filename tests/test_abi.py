@@ -115,10 +115,12 @@ def test_misaligned_pointers_rejected(lib):
 
 
 @pytest.mark.parametrize("kw,dense,name", [
-    ({}, False, "k_attn_w64<false>"),
-    ({}, True, "k_attn_w64<true>"),
-    ({"n_text": 256, "batch": 2, "heads": 24}, False, "k_attn_w64<false>"),
-    ({"grid_h": 128, "grid_w": 128, "tile": 16, "head_dim": 128, "keep": 7}, False, "k_attn_bf16<128, 4>"),
+    ({}, False, "k_attn_mfma<64, 3, false>"),
+    ({}, True, "k_attn_mfma<64, 3, true>"),
+    ({"n_text": 256, "batch": 2, "heads": 24}, False, "k_attn_mfma<64, 3, false>"),
+    ({"grid_h": 128, "grid_w": 128, "tile": 16, "head_dim": 128, "keep": 7}, False, "k_attn_mfma<128, 4, false>"),
+    ({"grid_h": 128, "grid_w": 128, "tile": 16, "head_dim": 128, "keep": 7}, True, "k_attn_mfma<128, 3, true>"),
+    ({"grid_h": 64, "grid_w": 64, "tile": 16, "keep": 4}, False, "k_attn_mfma<64, 4, false>"),
     ({"grid_h": 16, "grid_w": 16, "tile": 4, "keep": 4, "dtype": _lib.DT_F32}, False, "k_attn_f32<64>"),
     ({"grid_h": 32, "grid_w": 32, "tile": 4, "keep": 4}, False, "k_attn_bf16<64, 2>"),
 ])
@@ -128,5 +130,5 @@ def test_forward_kernel_names(lib, kw, dense, name):
 
 def test_forward_kernel_name_of_invalid_descriptor(lib):
     assert _lib.forward_kernel(_desc(keep=0)) is None
-    assert _lib.forward_kernel(_desc(keep=0), dense=True) == "k_attn_w64<true>"
+    assert _lib.forward_kernel(_desc(keep=0), dense=True) == "k_attn_mfma<64, 3, true>"
     assert _lib.forward_kernel(_desc(head_dim=96)) is None
