@@ -50,7 +50,11 @@ COPY_BYTES = 256 << 20
 # FETCH_SIZE and WRITE_SIZE in KiB per dispatch, and the copy calibration
 # factors (bytes known / bytes the counter reads for a plain 256 MiB copy).
 # From the counter summary in profiles/k_attn_mfma_grid64.md.
-MEASURED_TRAFFIC = {}
+MEASURED_TRAFFIC = {
+    ("k_attn_mfma<64, 3, false>", "grid64"): {"sha": "0da3378c879da633", "fetch_kib": 12500.1,
+                                              "write_kib": 8192.0, "fetch_factor": 1.9998,
+                                              "write_factor": 1.0},
+}
 
 
 def kernel_sources(kernel: str):
