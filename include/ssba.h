@@ -127,11 +127,25 @@ ssba_status ssba_forward(const ssba_desc* d, const void* q, const void* k, const
 ssba_status ssba_forward_dense(const ssba_desc* d, const void* q, const void* k, const void* v,
                                void* o, void* hip_stream);
 
-/* Name of the attention kernel that ssba_forward (dense = 0) or
- * ssba_forward_dense (dense != 0) launches for this descriptor, as profilers
- * show it without namespace and arguments (e.g. "k_attn_w64<false>"); NULL if
- * the descriptor is invalid.  Static storage; launches nothing. */
-const char* ssba_forward_kernel(const ssba_desc* d, int dense);
+/* Gate and attention in one call (the top-k gate fused into the attention
+ * kernel, Section 2.2.1 and Algorithm 1 pool through attend steps): the same
+ * results as ssba_build_index followed by ssba_forward -- `index` receives
+ * bit-identical index rows, `scratch` the same status flags, `o` the same
+ * output -- with one pass fewer over Q.  d->gate must be SSBA_GATE_TOPK.
+ * For bf16 inputs with 8x8 blocks, head_dim 64 or 128 and at most 64 blocks
+ * it launches a pooling kernel for K only and an attention kernel in which
+ * each query block pools its own queries, forms its affinity row and ranks
+ * it before attending; other shapes run the two calls.  Buffers, sizes and
+ * alignment as for ssba_build_index and ssba_forward. */
+ssba_status ssba_forward_topk(const ssba_desc* d, const void* q, const void* k, const void* v,
+                              int32_t* index, void* scratch, void* o, void* hip_stream);
+
+/* Name of the attention kernel that ssba_forward (mode 0), ssba_forward_dense
+ * (mode 1) or ssba_forward_topk (mode 2) launches for this descriptor, as
+ * profilers show it without namespace and arguments (e.g.
+ * "k_attn_mfma<64, 3, false, false>"); NULL if the descriptor or mode is
+ * invalid.  Static storage; launches nothing. */
+const char* ssba_forward_kernel(const ssba_desc* d, int mode);
 
 /* Synchronizes `hip_stream`, then reads the status flags that the last
  * ssba_build_index left in `scratch` (same descriptor): SSBA_OK, or

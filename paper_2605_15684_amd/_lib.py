@@ -27,7 +27,7 @@ GATE_DENSE = 2
 
 EXPORTS = ("ssba_abi_version", "ssba_status_str", "ssba_workspace_size", "ssba_build_index",
            "ssba_forward", "ssba_forward_dense", "ssba_read_device_status",
-           "ssba_forward_kernel")
+           "ssba_forward_kernel", "ssba_forward_topk")
 
 
 class SsbaDesc(ctypes.Structure):
@@ -83,6 +83,8 @@ def load(path: str = None) -> ctypes.CDLL:
     lib.ssba_forward.argtypes = [dp, vp, vp, vp, vp, vp, vp]
     lib.ssba_forward_dense.restype = ctypes.c_int
     lib.ssba_forward_dense.argtypes = [dp, vp, vp, vp, vp, vp]
+    lib.ssba_forward_topk.restype = ctypes.c_int
+    lib.ssba_forward_topk.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp]
     lib.ssba_forward_kernel.restype = ctypes.c_char_p
     lib.ssba_forward_kernel.argtypes = [dp, ctypes.c_int]
     lib.ssba_read_device_status.restype = ctypes.c_int
@@ -126,7 +128,14 @@ def read_device_status(desc, scratch_ptr, stream):
     return out.value
 
 
-def forward_kernel(desc, dense: bool = False):
-    """Name of the kernel ssba_forward (or ssba_forward_dense) would launch."""
-    name = load().ssba_forward_kernel(ctypes.byref(desc), 1 if dense else 0)
+def forward_topk(desc, q_ptr, k_ptr, v_ptr, index_ptr, scratch_ptr, o_ptr, stream) -> int:
+    return load().ssba_forward_topk(ctypes.byref(desc), q_ptr, k_ptr, v_ptr, index_ptr, scratch_ptr,
+                                    o_ptr, stream)
+
+
+def forward_kernel(desc, dense: bool = False, mode: int = None):
+    """Name of the kernel ssba_forward (mode 0), ssba_forward_dense (mode 1,
+    or dense=True) or ssba_forward_topk (mode 2) would launch."""
+    m = (1 if dense else 0) if mode is None else mode
+    name = load().ssba_forward_kernel(ctypes.byref(desc), m)
     return None if name is None else name.decode()

@@ -26,7 +26,7 @@ SOURCES = {
     "ssba_attn_f32.hip": [],
     # MFMA results in ordinary VGPRs: the softmax reads every score and the
     # default accumulation-register form costs a copy per element.
-    "ssba_attn_mfma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "ssba_attn_mfma.hip": ["-ffp-contract=off", "-mllvm", "-amdgpu-mfma-vgpr-form"],
 }
 
 COMMON = [

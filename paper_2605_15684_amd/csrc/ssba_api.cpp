@@ -172,17 +172,12 @@ ssba_status ssba_workspace_size(const ssba_desc* d, size_t* index_bytes, size_t*
   return SSBA_OK;
 }
 
-ssba_status ssba_build_index(const ssba_desc* d, const void* q, const void* k, int32_t* index,
-                             void* scratch, void* stream) {
-  Shape s;
-  const ssba_status st = check_desc(d, &s);
-  if (st != SSBA_OK) return st;
-  if (!index || !scratch || !aligned(index, 4) || !aligned(scratch, 16)) return SSBA_ERR_ARG;
-  const bool topk = d->gate == SSBA_GATE_TOPK;
-  if (topk) {
-    const size_t al = d->dtype == SSBA_DT_BF16 ? 16 : 4;
-    if (!q || !k || !aligned(q, al) || !aligned(k, al)) return SSBA_ERR_ARG;
-  }
+}  // extern "C"
+
+namespace {
+
+IndexArgs index_args(const ssba_desc* d, const Shape& s, const void* q, const void* k, int32_t* index,
+                     void* scratch, bool topk) {
   IndexArgs a;
   std::memset(&a, 0, sizeof(a));
   a.q = q;
@@ -205,6 +200,31 @@ ssba_status ssba_build_index(const ssba_desc* d, const void* q, const void* k, i
   a.win_w = d->win_w;
   a.ny = s.ny;
   a.f = s.f;
+  return a;
+}
+
+// Shapes whose top-k gate can run inside the attention kernel.
+bool gated_supported(const ssba_desc* d, const Shape& s) {
+  return d->dtype == SSBA_DT_BF16 && d->tile == 8 &&
+         ssba::mfma_supported(d->head_dim, 8, false, s.n_tiles, s.seq, (int64_t)s.seq * s.st);
+}
+
+}  // namespace
+
+extern "C" {
+
+ssba_status ssba_build_index(const ssba_desc* d, const void* q, const void* k, int32_t* index,
+                             void* scratch, void* stream) {
+  Shape s;
+  const ssba_status st = check_desc(d, &s);
+  if (st != SSBA_OK) return st;
+  if (!index || !scratch || !aligned(index, 4) || !aligned(scratch, 16)) return SSBA_ERR_ARG;
+  const bool topk = d->gate == SSBA_GATE_TOPK;
+  if (topk) {
+    const size_t al = d->dtype == SSBA_DT_BF16 ? 16 : 4;
+    if (!q || !k || !aligned(q, al) || !aligned(k, al)) return SSBA_ERR_ARG;
+  }
+  const IndexArgs a = index_args(d, s, q, k, index, scratch, topk);
   hipStream_t hs = static_cast<hipStream_t>(stream);
   hipError_t e;
   if (topk) {
@@ -216,10 +236,42 @@ ssba_status ssba_build_index(const ssba_desc* d, const void* q, const void* k, i
   return e == hipSuccess ? SSBA_OK : SSBA_ERR_HIP;
 }
 
-const char* ssba_forward_kernel(const ssba_desc* d, int dense) {
+ssba_status ssba_forward_topk(const ssba_desc* d, const void* q, const void* k, const void* v,
+                              int32_t* index, void* scratch, void* o, void* stream) {
   Shape s;
-  if (check_desc(d, &s, !dense) != SSBA_OK) return nullptr;
-  const AttnArgs a = attn_args(d, s, nullptr, nullptr, nullptr, nullptr, nullptr, dense != 0);
+  ssba_status st = check_desc(d, &s);
+  if (st != SSBA_OK) return st;
+  if (d->gate != SSBA_GATE_TOPK) return SSBA_ERR_ARG;
+  if (!q || !k || !v || !o || !index || !scratch) return SSBA_ERR_ARG;
+  const size_t al = d->dtype == SSBA_DT_BF16 ? 16 : 4;
+  if (!aligned(q, al) || !aligned(k, al) || !aligned(v, al) || !aligned(o, al) || !aligned(index, 4) ||
+      !aligned(scratch, 16))
+    return SSBA_ERR_ARG;
+  if (!gated_supported(d, s)) {   // the two calls, same results
+    st = ssba_build_index(d, q, k, index, scratch, stream);
+    return st != SSBA_OK ? st : ssba_forward(d, q, k, v, index, o, stream);
+  }
+  IndexArgs ia = index_args(d, s, q, k, index, scratch, true);
+  AttnArgs aa = attn_args(d, s, q, k, v, nullptr, o, false);
+  aa.gated = 1;
+  aa.keep = d->keep;
+  aa.qb = ia.qb;
+  aa.kb = ia.kb;
+  aa.index_out = index;
+  aa.flags = ia.flags;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  hipError_t e = ssba::launch_pool(ia, d->dtype, hs);
+  if (e == hipSuccess) e = ssba::launch_attn_bf16(aa, d->head_dim, d->tile, hs);
+  return e == hipSuccess ? SSBA_OK : SSBA_ERR_HIP;
+}
+
+const char* ssba_forward_kernel(const ssba_desc* d, int mode) {
+  Shape s;
+  const bool dense = mode == 1;
+  if (mode < 0 || mode > 2 || check_desc(d, &s, !dense) != SSBA_OK) return nullptr;
+  if (mode == 2 && d->gate != SSBA_GATE_TOPK) return nullptr;
+  AttnArgs a = attn_args(d, s, nullptr, nullptr, nullptr, nullptr, nullptr, dense);
+  a.gated = (mode == 2 && gated_supported(d, s)) ? 1 : 0;
   return ssba::attn_kernel_name(a, d->head_dim, d->tile, d->dtype);
 }
 

@@ -17,8 +17,8 @@
 //     (buffer_load_dwordx4 ... lds; the two waves of a stream split it), into
 //     double-buffered LDS.  Row offsets are scalar operands and the per-lane
 //     part is one VGPR per copy instruction and chunk, so a copy costs almost
-//     no vector ALU work.  Out-of-range rows read as zeros (the buffer bound
-//     is the (batch, head) slice);
+//     no vector ALU work (every row is a grid row by construction: kept block
+//     ids are range-checked before use);
 //   * the softmax is optimistic: probabilities are taken against the running
 //     max; only when a lane's chunk sum exceeds 2^20 (the max grew, or the
 //     first chunk) is the chunk max taken, O and l rescaled and the chunk
@@ -124,8 +124,109 @@ __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2{lo, hi}, bf16x2));
 }
 
+// Q^T operand of one query row: fragment ks holds channels 16 ks + 8 hw + [0, 8).
+template <int NKS>
+__device__ __forceinline__ void load_q(bf16x8 (&qf)[NKS], const u16* qbase, int qrow, int st, int hw) {
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks)
+    qf[ks] = *reinterpret_cast<const bf16x8*>(qbase + max(qrow, 0) * st + 16 * ks + 8 * hw);
+}
+
+// Kept block ids of the current workgroup's gate, ascending (gated launches).
+__shared__ int gate_list[64];
+
+// Affinity of one query block with key block `lane` (Eq. 2 on pooled sums):
+// the channel-ordered fp64 sum of the rounded products qsum[c] * kb[c][lane],
+// from the head's pooled key sums copied contiguously into the four buffers
+// (channel row c of T_b values in buffer c / (D/4)).  STRIDE = 64 gives every
+// read a constant offset; 0 reads with the runtime row length tb.  Lanes past
+// tb read a neighbouring row and are discarded by the caller.
+template <int D, int STRIDE>
+__device__ __forceinline__ double affinity(const double* qsum, const char* b0, const char* b1,
+                                           const char* b2, const char* b3, int lane, int tb) {
+  constexpr int CPQ = D / 4;
+  const int row = STRIDE ? STRIDE : tb;
+  double s = 0.0;
+#pragma unroll
+  for (int c = 0; c < D; ++c) {
+    const int qi = c / CPQ, cc = c % CPQ;
+    const char* src = qi == 0 ? b0 : qi == 1 ? b1 : qi == 2 ? b2 : b3;
+    const double kv = reinterpret_cast<const double*>(src)[cc * row + lane];
+    const double p = __dmul_rn(qsum[c], kv);
+    s = (c == 0) ? p : __dadd_rn(s, p);
+  }
+  return s;
+}
+
+// Top-k gate of query block i inside a gated launch (Section 2.2.1, Block
+// Compression / Affinity Matrix / Top-k Gating; Algorithm 1 pool, affinity and
+// top-k steps), with the arithmetic of the separate gate kernels so the index
+// rows are bit-identical to theirs:
+//   1. the head's pooled key sums [D][T_b] are copied into the four K/V
+//      buffers (a quarter of the channels each; they are free until the
+//      first chunk is copied);
+//   2. threads c < D fetch channel c of the block's pooled query sum (the
+//      pool kernel of the same call wrote both sums);
+//   3. wave 0, lane j < T_b: S[i][j] = sum over channels, in order, of the
+//      rounded products; then the wave's radix select picks the keep largest.
+// Writes the index row and status flag of block i; returns the kept count
+// with the ids in gate_list.  Every wave of the workgroup calls it.
+template <int D>
+__device__ __forceinline__ int gate_block(const AttnArgs& a, int bh, int i, int w, int lane,
+                                          char* b0, char* b1, char* b2, char* b3) {
+  __shared__ double qsum[D];
+  const int tb = a.n_tiles;
+  const int quarter_bytes = 2 * D * tb;   // D * tb * 8 / 4
+  // 1. pooled key sums of this (batch, head): wave w copies quarter w.
+  {
+    // The whole offset goes in the range-checked lane operand: bytes past the
+    // head's slice (a partial last copy) read as zeros.
+    const double* kbh = a.kb + (int64_t)bh * D * tb;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<double*>(kbh), (short)0, 4 * quarter_bytes, 0x00020000);
+    char* dst = w == 0 ? b0 : w == 1 ? b1 : w == 2 ? b2 : b3;
+    for (int o = 0; o < quarter_bytes; o += 1024)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(dst + o), 16,
+                                               (unsigned)(w * quarter_bytes + o + 16 * lane), 0u, 0, 0);
+  }
+  // 2. pooled query sums of block i, channel c = thread id.
+  const int tid = 64 * w + lane;
+  if (tid < D) qsum[tid] = a.qb[((int64_t)bh * tb + i) * D + tid];
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  __syncthreads();
+  // 3. affinity row and ranking (wave 0).
+  if (w == 0) {
+    const bool valid = lane < tb;
+    const double s = tb == 64 ? affinity<D, 64>(qsum, b0, b1, b2, b3, lane, tb)
+                              : affinity<D, 0>(qsum, b0, b1, b2, b3, lane, tb);
+    const uint64_t key = valid ? rank_key(s) : 0;
+    const bool kept = wave_topk(key, valid, a.keep, lane);
+    const uint64_t km = __builtin_amdgcn_ballot_w64(kept);
+    const int pos = __popcll(km & ((1ull << lane) - 1ull));
+    const bool bad = __builtin_amdgcn_ballot_w64(valid && !isfinite(s)) != 0;
+    int32_t* out = a.index_out + ((int64_t)bh * tb + i) * (tb + 1);
+    if (valid) {
+      if (kept) {
+        gate_list[pos] = lane;
+        out[1 + pos] = lane;
+      }
+      if (lane >= a.keep) out[1 + lane] = -1;
+    }
+    if (lane == 0) {
+      out[0] = a.keep;
+      a.flags[(int64_t)bh * tb + i] = bad ? 1 : 0;
+    }
+  }
+  // The list is published, and every wave is past the pooled sums before
+  // the first chunk is copied over them.
+  __syncthreads();
+  return a.keep;
+}
+
 // DENSE: every group runs natural-order rows over all keys (no index).
-template <int D, int TILE_LOG2, bool DENSE>
+// GATED: each image group computes its block's top-k gate first (from the
+// pooled key sums) and writes the block's index row and status flag.
+template <int D, int TILE_LOG2, bool DENSE, bool GATED>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 64 ? 4 : 2)))
 k_attn_mfma(AttnArgs a) {
   using S = Shape<D, TILE_LOG2>;
@@ -181,6 +282,7 @@ k_attn_mfma(AttnArgs a) {
 
   Plan p;
   int qrow;
+  bf16x8 qf[NKS];   // Q^T operand [ks]: query 32 qh + l32, channels 16 ks + 8 hw + [0, 8)
   int listv = -1;   // lane e holds kept block id number e (image groups)
   if (DENSE || r < a.n_text_groups) {   // natural order: text rows, or every row
     const int end = DENSE ? a.seq : a.f.n_text;
@@ -193,20 +295,23 @@ k_attn_mfma(AttnArgs a) {
     const int g = r - a.n_text_groups;     // image group: block i, quarter gq
     const int i = g / GPB, gq = g - i * GPB;
     qrow = frame_row(a.f, i, 64 * gq + 32 * qh + l32);
-    const int32_t* list = a.index + (bh * (int64_t)a.n_tiles + i) * (a.n_tiles + 1);
-    const int count = min(max(list[0], 0), min(a.n_tiles, 64));
-    const int e = lane < count ? list[1 + lane] : 0;
+    int count, e;
+    if constexpr (GATED) {
+      load_q<NKS>(qf, qbase, qrow, st, hw);   // in flight during the gate
+      count = gate_block<D>(a, bh, i, w, lane, kA, kB, vA, vB);
+      e = lane < count ? gate_list[lane] : 0;
+    } else {
+      const int32_t* list = a.index + (bh * (int64_t)a.n_tiles + i) * (a.n_tiles + 1);
+      count = min(max(list[0], 0), min(a.n_tiles, 64));
+      e = lane < count ? list[1 + lane] : 0;
+    }
     listv = (unsigned)e < (unsigned)a.n_tiles ? e : -1;
     p.img_chunks = CPB * count;
     p.natural_end = 0;
     p.n_chunks = p.img_chunks + (a.f.n_text + KC - 1) / KC;
   }
 
-  // Q^T operand [ks]: query 32 qh + l32, channels 16 ks + 8 hw + [0, 8).
-  bf16x8 qf[NKS];
-#pragma unroll
-  for (int ks = 0; ks < NKS; ++ks)
-    qf[ks] = *reinterpret_cast<const bf16x8*>(qbase + max(qrow, 0) * st + 16 * ks + 8 * hw);
+  if (!GATED || DENSE || r < a.n_text_groups) load_q<NKS>(qf, qbase, qrow, st, hw);
 
   // Buffer resources over this (batch, head) slice: rows [0, seq).
   const unsigned slice_bytes = 2u * (unsigned)((a.seq - 1) * st + D);
@@ -477,12 +582,13 @@ k_attn_mfma(AttnArgs a) {
 
 }  // namespace
 
-const char* mfma_kernel_name(int head_dim, int tile, bool dense) {
+const char* mfma_kernel_name(int head_dim, int tile, bool dense, bool gated) {
   static const char* const names[2][2][2] = {
-      {{"k_attn_mfma<64, 3, false>", "k_attn_mfma<64, 3, true>"},
-       {"k_attn_mfma<64, 4, false>", "k_attn_mfma<64, 4, true>"}},
-      {{"k_attn_mfma<128, 3, false>", "k_attn_mfma<128, 3, true>"},
-       {"k_attn_mfma<128, 4, false>", "k_attn_mfma<128, 4, true>"}}};
+      {{"k_attn_mfma<64, 3, false, false>", "k_attn_mfma<64, 3, true, false>"},
+       {"k_attn_mfma<64, 4, false, false>", "k_attn_mfma<64, 4, true, false>"}},
+      {{"k_attn_mfma<128, 3, false, false>", "k_attn_mfma<128, 3, true, false>"},
+       {"k_attn_mfma<128, 4, false, false>", "k_attn_mfma<128, 4, true, false>"}}};
+  if (gated && !dense) return head_dim == 64 ? "k_attn_mfma<64, 3, false, true>" : "k_attn_mfma<128, 3, false, true>";
   // The dense control runs natural-order rows only; it uses the 8x8 shape.
   const int ti = (!dense && tile == 16) ? 1 : 0;
   return names[head_dim == 64 ? 0 : 1][ti][dense ? 1 : 0];
@@ -511,14 +617,17 @@ hipError_t launch_attn_mfma(const AttnArgs& a0, int head_dim, int tile, hipStrea
   if (total <= 0) return hipSuccess;
   const dim3 grid((unsigned)total), block(256);
   const bool big = !a.dense && tile == 16;
+  if (a.gated && (a.dense || big)) return hipErrorInvalidValue;   // gated: 8x8 blocks only
   if (head_dim == 64) {
-    if (a.dense) hipLaunchKernelGGL((k_attn_mfma<64, 3, true>), grid, block, 0, s, a);
-    else if (big) hipLaunchKernelGGL((k_attn_mfma<64, 4, false>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((k_attn_mfma<64, 3, false>), grid, block, 0, s, a);
+    if (a.dense) hipLaunchKernelGGL((k_attn_mfma<64, 3, true, false>), grid, block, 0, s, a);
+    else if (a.gated) hipLaunchKernelGGL((k_attn_mfma<64, 3, false, true>), grid, block, 0, s, a);
+    else if (big) hipLaunchKernelGGL((k_attn_mfma<64, 4, false, false>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((k_attn_mfma<64, 3, false, false>), grid, block, 0, s, a);
   } else {
-    if (a.dense) hipLaunchKernelGGL((k_attn_mfma<128, 3, true>), grid, block, 0, s, a);
-    else if (big) hipLaunchKernelGGL((k_attn_mfma<128, 4, false>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((k_attn_mfma<128, 3, false>), grid, block, 0, s, a);
+    if (a.dense) hipLaunchKernelGGL((k_attn_mfma<128, 3, true, false>), grid, block, 0, s, a);
+    else if (a.gated) hipLaunchKernelGGL((k_attn_mfma<128, 3, false, true>), grid, block, 0, s, a);
+    else if (big) hipLaunchKernelGGL((k_attn_mfma<128, 4, false, false>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((k_attn_mfma<128, 3, false, false>), grid, block, 0, s, a);
   }
   return hipGetLastError();
 }

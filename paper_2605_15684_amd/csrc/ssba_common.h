@@ -31,6 +31,42 @@ __host__ __device__ __forceinline__ int frame_row(const Frame& f, int t, int s) 
   return f.n_text + y * f.grid_w + x;
 }
 
+// Ranking key of the top-k gate: an unsigned integer whose order is the
+// gate's order on affinities.  -0 is folded onto +0 and every NaN onto key 0,
+// below all numbers; equal keys are then ordered by ascending block index.
+__device__ __forceinline__ uint64_t rank_key(double s) {
+  if (s != s) return 0;
+  if (s == 0.0) s = 0.0;
+  const uint64_t u = (uint64_t)__double_as_longlong(s);
+  return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
+}
+
+// Top-k selection over one wave (lane = block id < tb): true in the lanes of
+// the `keep` blocks ranked first by (key descending, block id ascending).
+// Radix select: the keep-th largest key is found bit by bit from the top
+// with wave ballots; keys above it are kept and, of the keys equal to it,
+// the lowest block ids fill the remaining places.  The search stops early
+// once exactly `keep` keys lie at or above the bits decided so far: that set
+// is then the answer.  Invalid lanes count as key 0, which no candidate
+// (always >= 1) reaches.
+__device__ __forceinline__ bool wave_topk(uint64_t key, bool valid, int keep, int lane) {
+  const uint64_t k = valid ? key : 0;
+  uint64_t thr = 0;
+#pragma unroll 4
+  for (int bit = 63; bit >= 0; --bit) {
+    const uint64_t cand = thr | (1ull << bit);
+    const int n = __popcll(__builtin_amdgcn_ballot_w64(k >= cand));
+    if (n >= keep) {
+      thr = cand;
+      if (n == keep) break;
+    }
+  }
+  const bool gt = valid && k > thr, eq = valid && k == thr;
+  const int need = keep - __popcll(__builtin_amdgcn_ballot_w64(gt));
+  const int before = __popcll(__builtin_amdgcn_ballot_w64(eq) & ((1ull << lane) - 1ull));
+  return gt || (eq && before < need);
+}
+
 // Everything an attention launch needs; passed by value as a kernel argument.
 struct AttnArgs {
   const void* q;
@@ -48,6 +84,14 @@ struct AttnArgs {
   int groups_per_tile;   // image workgroups per query block (tile^2 / rows per group)
   int groups_per_bh;     // workgroups per (batch, head)
   int dense;             // 1: every row attends every key in natural order
+  // Gated launches compute the top-k gate of each image block in the kernel
+  // from the pooled sums and write the index rows and status flags.
+  int gated;
+  int keep;
+  const double* qb;      // [B][H][T_b][D] pooled query sums
+  const double* kb;      // [B][H][D][T_b] pooled key sums
+  int32_t* index_out;    // [B][H][T_b][1 + T_b]
+  int32_t* flags;        // [B][H][T_b]
 };
 
 struct IndexArgs {
@@ -68,10 +112,11 @@ hipError_t launch_gate_topk(const IndexArgs& a, hipStream_t s);
 hipError_t launch_gate_static(const IndexArgs& a, int gate, hipStream_t s);
 hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, int tile, hipStream_t s);
 hipError_t launch_attn_f32(const AttnArgs& a, int head_dim, int tile, hipStream_t s);
-// One-wave-per-64-rows bf16 kernel for head_dim 64 (8x8 blocks or dense).
+// Four-wave MFMA kernel: head_dim 64 / 128, 8x8 / 16x16 blocks, dense control;
+// gated launches (a.gated) need 8x8 blocks.
 bool mfma_supported(int head_dim, int tile, bool dense, int n_tiles, int seq, int64_t span);
 hipError_t launch_attn_mfma(const AttnArgs& a, int head_dim, int tile, hipStream_t s);
-const char* mfma_kernel_name(int head_dim, int tile, bool dense);
+const char* mfma_kernel_name(int head_dim, int tile, bool dense, bool gated);
 // Name of the kernel launch_attn_bf16 / launch_attn_f32 would run.
 const char* attn_kernel_name(const AttnArgs& a, int head_dim, int tile, int dtype);
 

@@ -52,14 +52,15 @@ __global__ void __launch_bounds__(256) k_pool(IndexArgs a) {
   constexpr bool BF16 = DTYPE == SSBA_DT_BF16;
   constexpr int EPV = BF16 ? 8 : 1;                    // elements per load
   constexpr int VPR = D / EPV;                         // loads per token row
-  constexpr int LOADS = 2 * SB * VPR;                  // per stage, Q then K
+  constexpr int NT = 2;                                // tensors pooled
+  constexpr int LOADS = NT * SB * VPR;                 // per stage, Q then K
   using Vec = typename std::conditional<BF16, uint4, float>::type;
   __shared__ Vec stage[LOADS];
   int t, h, b;
   unit_of(a, t, h, b);
   const int tid = threadIdx.x;
   const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
-  const int which = tid / D, c = tid % D;              // summing threads: tid < 2D
+  const int which = tid / D, c = tid % D;              // summing threads: tid < NT D
   double sum = 0.0;
 #pragma unroll 1
   for (int s0 = 0; s0 < SLOTS; s0 += SB) {
@@ -77,7 +78,7 @@ __global__ void __launch_bounds__(256) k_pool(IndexArgs a) {
 #pragma unroll
     for (int r = 0; r < LOADS / 256; ++r) stage[tid + 256 * r] = v[r];
     __syncthreads();
-    if (tid < 2 * D) {
+    if (tid < NT * D) {
       const char* col = reinterpret_cast<const char*>(stage) +
                         ((size_t)which * SB * D + c) * (BF16 ? 2 : 4);
       // Every staged value of the chain is read before the first add, so
@@ -98,23 +99,13 @@ __global__ void __launch_bounds__(256) k_pool(IndexArgs a) {
     }
     __syncthreads();
   }
-  if (tid < 2 * D) {
+  if (tid < NT * D) {
     const int64_t bh = (int64_t)b * a.heads + h;
     if (which == 0)
       a.qb[(bh * a.n_tiles + t) * D + c] = sum;
     else
       a.kb[(bh * D + c) * a.n_tiles + t] = sum;
   }
-}
-
-// Ranking key: an unsigned integer whose order is the gate's order on
-// affinities.  -0 is folded onto +0 and every NaN onto key 0, below all
-// numbers; equal keys are then ordered by ascending block index.
-__device__ __forceinline__ uint64_t rank_key(double s) {
-  if (s != s) return 0;
-  if (s == 0.0) s = 0.0;
-  const uint64_t u = (uint64_t)__double_as_longlong(s);
-  return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
 }
 
 // One workgroup per query block (i, h, b); thread j computes S[i][j] (the
@@ -158,21 +149,7 @@ __global__ void __launch_bounds__(MAXT) k_gate_topk(IndexArgs a) {
   __syncthreads();
   bool kept = false;
   if (MAXT == 64) {
-    // One wave holds every key.  Radix select: T is the largest value with
-    // at least `keep` keys >= T (the keep-th largest key), found bit by bit
-    // from the top with wave ballots; keys above T are kept, and of the keys
-    // equal to T the lowest block ids fill the remaining places.
-    const bool valid = j < tb;
-    uint64_t thr = 0;
-#pragma unroll 8
-    for (int bit = 63; bit >= 0; --bit) {
-      const uint64_t cand = thr | (1ull << bit);
-      if (__popcll(__ballot(valid && key >= cand)) >= a.keep) thr = cand;
-    }
-    const bool gt = valid && key > thr, eq = valid && key == thr;
-    const int need = a.keep - __popcll(__ballot(gt));
-    const int before = __popcll(__ballot(eq) & ((1ull << lane) - 1ull));
-    kept = gt || (eq && before < need);
+    kept = wave_topk(key, j < tb, a.keep, lane);   // one wave holds every key
   } else if (j < tb) {
     int rank = 0;
     for (int jj = 0; jj < tb; ++jj) {

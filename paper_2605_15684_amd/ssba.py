@@ -146,6 +146,26 @@ def forward_dense(q, k, v, desc, out=None):
     return out
 
 
+def forward_topk(q, k, v, desc, index=None, scratch=None, out=None):
+    """Top-k gate and attention in one call (gate fused into the attention
+    kernel where the shape allows).  Returns (index, scratch, out); index and
+    scratch hold exactly what build_index would have left there."""
+    if desc.gate != _lib.GATE_TOPK:
+        raise ValueError("forward_topk needs the top-k gate")
+    if out is None:
+        out = torch.empty_strided(q.shape, q.stride(), dtype=q.dtype, device=q.device)
+    _check_tensors(desc, q, k, v, out)
+    if index is None or scratch is None:
+        index, scratch = alloc_workspace(desc, q.device)
+    ib, sb = _lib.workspace_size(desc)
+    if not (index.is_cuda and scratch.is_cuda and index.dtype == torch.int32 and index.is_contiguous()
+            and index.numel() * 4 >= ib and scratch.numel() * scratch.element_size() >= sb):
+        raise ValueError("index / scratch buffers too small or not on the GPU")
+    _lib.check(_lib.forward_topk(desc, q.data_ptr(), k.data_ptr(), v.data_ptr(), index.data_ptr(),
+                                 scratch.data_ptr(), out.data_ptr(), _stream(q.device)), "ssba_forward_topk")
+    return index, scratch, out
+
+
 def read_status(desc, scratch) -> int:
     """Synchronize and return SSBA_OK or SSBA_ERR_NONFINITE from the last gate."""
     return _lib.read_device_status(desc, scratch.data_ptr(), _stream(scratch.device))
@@ -166,6 +186,9 @@ def attention(q, k, v, *, grid, tile, shift=None, layer=None, rho=None, keep=Non
         keep = keep_from_rho(tb, 0.75 if rho is None else rho)
     desc = desc_for(q, grid=grid, tile=tile, shift=shift, n_text=n_text, gate=gate,
                     keep=keep or 0, window=window or (1, 1), scale=scale)
-    index, _ = build_index(q, k, desc)
-    o = forward(q, k, v, index, desc)
+    if gate == "topk":
+        _, _, o = forward_topk(q, k, v, desc)
+    else:
+        index, _ = build_index(q, k, desc)
+        o = forward(q, k, v, index, desc)
     return o if return_text else o[:, :, n_text:]

@@ -115,12 +115,12 @@ def test_misaligned_pointers_rejected(lib):
 
 
 @pytest.mark.parametrize("kw,dense,name", [
-    ({}, False, "k_attn_mfma<64, 3, false>"),
-    ({}, True, "k_attn_mfma<64, 3, true>"),
-    ({"n_text": 256, "batch": 2, "heads": 24}, False, "k_attn_mfma<64, 3, false>"),
-    ({"grid_h": 128, "grid_w": 128, "tile": 16, "head_dim": 128, "keep": 7}, False, "k_attn_mfma<128, 4, false>"),
-    ({"grid_h": 128, "grid_w": 128, "tile": 16, "head_dim": 128, "keep": 7}, True, "k_attn_mfma<128, 3, true>"),
-    ({"grid_h": 64, "grid_w": 64, "tile": 16, "keep": 4}, False, "k_attn_mfma<64, 4, false>"),
+    ({}, False, "k_attn_mfma<64, 3, false, false>"),
+    ({}, True, "k_attn_mfma<64, 3, true, false>"),
+    ({"n_text": 256, "batch": 2, "heads": 24}, False, "k_attn_mfma<64, 3, false, false>"),
+    ({"grid_h": 128, "grid_w": 128, "tile": 16, "head_dim": 128, "keep": 7}, False, "k_attn_mfma<128, 4, false, false>"),
+    ({"grid_h": 128, "grid_w": 128, "tile": 16, "head_dim": 128, "keep": 7}, True, "k_attn_mfma<128, 3, true, false>"),
+    ({"grid_h": 64, "grid_w": 64, "tile": 16, "keep": 4}, False, "k_attn_mfma<64, 4, false, false>"),
     ({"grid_h": 16, "grid_w": 16, "tile": 4, "keep": 4, "dtype": _lib.DT_F32}, False, "k_attn_f32<64>"),
     ({"grid_h": 32, "grid_w": 32, "tile": 4, "keep": 4}, False, "k_attn_bf16<64, 2>"),
 ])
@@ -128,7 +128,26 @@ def test_forward_kernel_names(lib, kw, dense, name):
     assert _lib.forward_kernel(_desc(**kw), dense) == name
 
 
+@pytest.mark.parametrize("kw,name", [
+    ({}, "k_attn_mfma<64, 3, false, true>"),
+    ({"n_text": 256, "batch": 2, "heads": 24}, "k_attn_mfma<64, 3, false, true>"),
+    ({"head_dim": 128}, "k_attn_mfma<128, 3, false, true>"),
+    ({"grid_h": 128, "grid_w": 128, "tile": 16, "head_dim": 128, "keep": 7}, "k_attn_mfma<128, 4, false, false>"),
+    ({"grid_h": 16, "grid_w": 16, "tile": 4, "keep": 4, "dtype": _lib.DT_F32}, "k_attn_f32<64>"),
+])
+def test_forward_topk_kernel_names(lib, kw, name):
+    assert _lib.forward_kernel(_desc(**kw), mode=2) == name
+
+
+def test_forward_topk_rejects_other_gates_before_launch(lib):
+    d = _desc(gate=_lib.GATE_WINDOW, win_h=2, win_w=2)
+    buf = ctypes.c_void_p(256)   # never dereferenced: the descriptor is rejected first
+    assert lib.ssba_forward_topk(ctypes.byref(d), buf, buf, buf, buf, buf, buf, None) == _lib.SSBA_ERR_ARG
+    assert _lib.forward_kernel(d, mode=2) is None
+    assert _lib.forward_kernel(_desc(), mode=3) is None
+
+
 def test_forward_kernel_name_of_invalid_descriptor(lib):
     assert _lib.forward_kernel(_desc(keep=0)) is None
-    assert _lib.forward_kernel(_desc(keep=0), dense=True) == "k_attn_mfma<64, 3, true>"
+    assert _lib.forward_kernel(_desc(keep=0), dense=True) == "k_attn_mfma<64, 3, true, false>"
     assert _lib.forward_kernel(_desc(head_dim=96)) is None

@@ -34,7 +34,7 @@ def test_more_than_one_gpu_is_refused():
 
 
 def test_traffic_only_for_the_measured_sources(monkeypatch):
-    key = ("k_attn_mfma<64, 3, false>", "grid64")
+    key = ("k_attn_mfma<64, 3, false, false>", "grid64")
     entry = {"sha": "", "fetch_kib": 12000.0, "write_kib": 8192.0, "fetch_factor": 2.0, "write_factor": 1.0}
     monkeypatch.setitem(bench.MEASURED_TRAFFIC, key, dict(entry, sha=bench.sources_sha(key[0])))
     t = bench.measured_traffic(*key)

@@ -10,7 +10,7 @@ from paper_2605_15684_amd.inputs import (PRESETS, SWEEP_TOPK_KEEP, SWEEP_WINDOW,
                                          preset, workload_from)
 
 from _parity import (BF16_TOL, F32_TOL, gpu_desc, inputs, max_err, oracle_index, oracle_kw,
-                      run_gpu, sample_rows, to64, tol)
+                      run_gpu, sample_rows, to64, tol)  # noqa: F401
 
 pytestmark = pytest.mark.gpu
 
@@ -250,3 +250,62 @@ def test_graph_replay_matches_eager():
         assert torch.equal(index, ref_index), rep
         assert torch.equal(out, ref_out), rep
         assert eager_other.shape == out.shape
+
+
+TOPK_CASES = [
+    preset("grid64", heads=4),
+    preset("grid64", heads=2, shift=(-4, -4)),
+    preset("grid64_text", batch=1, heads=4),
+    workload_from(batch=1, heads=2, grid_h=32, grid_w=64, head_dim=128, tile=8, keep=5, shift=(4, -4),
+                  n_text=77),
+    workload_from(batch=2, heads=3, grid_h=48, grid_w=40, head_dim=64, tile=8, keep=7, shift=(3, 5),
+                  n_text=13),
+    preset("grid128", heads=2),                                  # 16x16 blocks: two-call route
+    preset("tiny"),                                              # fp32: two-call route
+]
+
+
+@pytest.mark.parametrize("w", TOPK_CASES, ids=_ids)
+def test_forward_topk_equals_build_index_then_forward(w):
+    """The fused gate writes bit-identical index rows and status flags, and the
+    attention output equals the two-call output bit for bit."""
+    from paper_2605_15684_amd import ssba
+    (_, _, _), (qg, kg, vg) = inputs(w)
+    desc = gpu_desc(w, qg)
+    index2, scratch2 = ssba.build_index(qg, kg, desc)
+    out2 = ssba.forward(qg, kg, vg, index2, desc)
+    index1, scratch1 = ssba.alloc_workspace(desc, qg.device)
+    index1.fill_(-5)
+    _, _, out1 = ssba.forward_topk(qg, kg, vg, desc, index1, scratch1)
+    torch.cuda.synchronize()
+    assert torch.equal(index1, index2)
+    assert ssba.read_status(desc, scratch1) == ssba.read_status(desc, scratch2) == 0
+    assert torch.equal(out1, out2)
+
+
+def test_forward_topk_full_size_against_oracle():
+    from paper_2605_15684_amd import ssba
+    w = preset("grid64")
+    (q, k, v), (qg, kg, vg) = inputs(w)
+    desc = gpu_desc(w, qg)
+    index, _, out = ssba.forward_topk(qg, kg, vg, desc)
+    torch.cuda.synchronize()
+    want_idx = oracle_index(w, q, k)
+    assert np.array_equal(index.cpu().numpy(), want_idx)
+    rng = np.random.default_rng(7)
+    heads = [(0, 0), (0, w.heads - 1), (0, int(rng.integers(w.heads)))]
+    rows = sample_rows(w, rng)
+    ref = O.attention(to64(q), to64(k), to64(v), want_idx, rows=rows, heads=heads, **oracle_kw(w))
+    err = max_err(out, ref, heads, rows)
+    assert err <= BF16_TOL, f"max-abs {err:.3e}"
+
+
+def test_forward_topk_nonfinite_sets_status():
+    from paper_2605_15684_amd import ssba
+    w = preset("grid64", heads=2)
+    (_, _, _), (qg, kg, vg) = inputs(w)
+    desc = gpu_desc(w, qg)
+    kg2 = kg.clone()
+    kg2[0, 1, 100, 5] = float("nan")
+    _, scratch, _ = ssba.forward_topk(qg, kg2, vg, desc)
+    assert ssba.read_status(desc, scratch) == 5
