@@ -12,8 +12,12 @@ same call as ssba_build_index + ssba_forward is timed too
 stream the library launches on, once launched eagerly and once replayed from
 a HIP graph captured from the same calls (same kernels, same work; the replay
 is checked bit-exact against the eager output); `value` uses the faster.
-Index, forward and dense launches are also timed separately, back to back.  Prints ONE JSON line on stdout; --sweep prints extra
-per-configuration lines on stderr (sparsity sweep, text tokens, 2K grid).
+Index, forward and dense launches are also timed separately, back to back.
+These are warm numbers (Q, K, V and O stay in the 256 MB MALL between
+calls); ms_step_cold and ms_fwd_cold are the median of ten single calls each
+made after a 1 GiB buffer is written, so the inputs come from HBM.  Prints
+ONE JSON line on stdout; --sweep prints extra per-configuration lines on
+stderr (sparsity sweep, text tokens, 2K grid).
 
 Flops are counted over computed (kept) query/key pairs only: 4 * D per pair
 (2 * D for Q K^T, 2 * D for P V).  Pairs per (batch, head):
@@ -171,6 +175,24 @@ class Runner:
         wall = (time.perf_counter() - t0) * 1e3 / steps
         return wall, ms
 
+    def cold_ms(self, fn, reps: int = 10) -> float:
+        """Median ms of one call of `fn` after a 1 GiB buffer is written, which
+        evicts Q, K, V and O from the 256 MB last-level cache (MALL)."""
+        torch = self.torch
+        if not hasattr(self, "_evict"):
+            self._evict = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+        times = []
+        for r in range(reps):
+            self._evict.fill_(float(r))
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1))
+        times.sort()
+        return times[len(times) // 2]
+
     def graph_step_ms(self, steps: int):
         """The same step captured once in a HIP graph and replayed."""
         torch = self.torch
@@ -238,6 +260,8 @@ def measure(w, steps: int, warmup: int, dense_steps: int, graph: bool = True):
     for _ in range(3):
         r.run_dense()
     dense_ms = r._span(r.run_dense, dense_steps)
+    cold_step_ms = r.cold_ms(r.step)
+    cold_fwd_ms = r.cold_ms(r.run_fwd)
     graph_ms = None
     if graph:
         graph_ms, g = r.graph_step_ms(steps)
@@ -252,7 +276,7 @@ def measure(w, steps: int, warmup: int, dense_steps: int, graph: bool = True):
     return r, {
         "ms_step_wall": wall_ms, "ms_step_eager": step_ms, "ms_step_graph": graph_ms,
         "ms_step": best_ms, "ms_step_two_calls": two_ms, "ms_index": idx_ms, "ms_fwd": fwd_ms,
-        "ms_dense": dense_ms, "gflop": f / 1e9, "gflop_dense": flops(w, dense=True) / 1e9,
+        "ms_dense": dense_ms, "ms_step_cold": cold_step_ms, "ms_fwd_cold": cold_fwd_ms, "gflop": f / 1e9, "gflop_dense": flops(w, dense=True) / 1e9,
         "tflops_fwd": f / (fwd_ms * 1e-3) / 1e12,
         "tflops_step": f / (best_ms * 1e-3) / 1e12,
         "tflops_dense": flops(w, dense=True) / (dense_ms * 1e-3) / 1e12,
@@ -311,6 +335,7 @@ def main():
         "ms_dense": round(m["ms_dense"], 5), "ms_step_wall": round(m["ms_step_wall"], 5),
         "ms_step_eager": round(m["ms_step_eager"], 5),
         "ms_step_two_calls": round(m["ms_step_two_calls"], 5),
+        "ms_step_cold": round(m["ms_step_cold"], 5), "ms_fwd_cold": round(m["ms_fwd_cold"], 5),
         "ms_step_graph": None if m["ms_step_graph"] is None else round(m["ms_step_graph"], 5),
         "tflops_fwd": round(m["tflops_fwd"], 2), "pct_peak_fwd": round(100 * m["tflops_fwd"] / PEAK_BF16_TFLOPS, 2),
         "tflops_dense": round(m["tflops_dense"], 2),

@@ -60,6 +60,7 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx2 __attribute__((ext_vector_type(2)));
+typedef float floatx8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef uint16_t u16;
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
@@ -130,6 +131,15 @@ __device__ __forceinline__ void load_q(bf16x8 (&qf)[NKS], const u16* qbase, int 
 #pragma unroll
   for (int ks = 0; ks < NKS; ++ks)
     qf[ks] = *reinterpret_cast<const bf16x8*>(qbase + max(qrow, 0) * st + 16 * ks + 8 * hw);
+}
+
+// Q^T operands scaled by softmax scale * log2(e) and rounded to bf16 (round
+// to nearest even), so a product Q K^T is already the exponent of exp2.
+template <int NKS>
+__device__ __forceinline__ void scale_q(bf16x8 (&qf)[NKS], float c2) {
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks)
+    qf[ks] = __builtin_convertvector(__builtin_convertvector(qf[ks], floatx8) * c2, bf16x8);
 }
 
 // Kept block ids of the current workgroup's gate, ascending (gated launches).
@@ -288,6 +298,7 @@ k_attn_mfma(AttnArgs a) {
     const int end = DENSE ? a.seq : a.f.n_text;
     const int q = r * 64 + 32 * qh + l32;
     qrow = q < end ? q : -1;
+    load_q<NKS>(qf, qbase, qrow, st, hw);
     p.img_chunks = 0;
     p.natural_end = a.seq;
     p.n_chunks = (a.seq + KC - 1) / KC;
@@ -295,23 +306,24 @@ k_attn_mfma(AttnArgs a) {
     const int g = r - a.n_text_groups;     // image group: block i, quarter gq
     const int i = g / GPB, gq = g - i * GPB;
     qrow = frame_row(a.f, i, 64 * gq + 32 * qh + l32);
+    load_q<NKS>(qf, qbase, qrow, st, hw);   // in flight during the gate or the list read
     int count, e;
     if constexpr (GATED) {
-      load_q<NKS>(qf, qbase, qrow, st, hw);   // in flight during the gate
       count = gate_block<D>(a, bh, i, w, lane, kA, kB, vA, vB);
       e = lane < count ? gate_list[lane] : 0;
     } else {
+      // The count and the entries are requested together (one round trip).
       const int32_t* list = a.index + (bh * (int64_t)a.n_tiles + i) * (a.n_tiles + 1);
-      count = min(max(list[0], 0), min(a.n_tiles, 64));
-      e = lane < count ? list[1 + lane] : 0;
+      const int raw = list[0];
+      const int ent = lane < a.n_tiles ? list[1 + lane] : 0;
+      count = min(max(raw, 0), min(a.n_tiles, 64));
+      e = lane < count ? ent : 0;
     }
     listv = (unsigned)e < (unsigned)a.n_tiles ? e : -1;
     p.img_chunks = CPB * count;
     p.natural_end = 0;
     p.n_chunks = p.img_chunks + (a.f.n_text + KC - 1) / KC;
   }
-
-  if (!GATED || DENSE || r < a.n_text_groups) load_q<NKS>(qf, qbase, qrow, st, hw);
 
   // Buffer resources over this (batch, head) slice: rows [0, seq).
   const unsigned slice_bytes = 2u * (unsigned)((a.seq - 1) * st + D);
@@ -435,15 +447,20 @@ k_attn_mfma(AttnArgs a) {
   floatx16 oacc[NDB];   // [db]
 #pragma unroll
   for (int db = 0; db < NDB; ++db) oacc[db] = floatx16{};
+  // Softmax state per query (the lane's): running max m_run of the scaled
+  // scores (-1e30 until a finite one is seen) and running sum l_run.  The
+  // score products start from negm = -m_run (0 while unset), so the common
+  // chunk feeds the accumulator straight into exp2.
   float m_run = -1e30f, l_run = 0.f;
-  const float c2 = a.scale_log2;
+  floatx16 negm = floatx16{};
+  scale_q<NKS>(qf, a.scale_log2);
   const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
 
   // One half chunk: K in kt, V in vt (this stream's halves), keys outside
   // [lo, hi) masked.
   auto step = [&](const char* kt, const char* vt, int lo, int hi) {
     // S^T = K . Q^T: the lane's 16 keys 8 (r / 4) + 4 hw + r % 4 of its query.
-    floatx16 sc = floatx16{};
+    floatx16 sc = negm;   // sc = s - m_run: the exponent of exp2 for this chunk
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
       const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kt + koff[ks]);
@@ -458,36 +475,42 @@ k_attn_mfma(AttnArgs a) {
         if (key < l4 || key >= h4) sc[rr] = -INFINITY;
       }
     }
-    // P = exp2(c2 S - m) as bf16 pairs and the lane's sum of the rounded P.
+    // P = exp2(sc - shift) as bf16 pairs and the lane's sum of the rounded P
+    // (shift is 0 except when a chunk is redone).
     uint32_t pk[8];
     float ls;
-    auto probs = [&]() {
-      const float mneg = -m_run;
+    auto probs = [&](float shift, bool shifted) {
       float ls0 = 0.f, ls1 = 0.f;
 #pragma unroll
       for (int rr = 0; rr < 16; rr += 2) {
-        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[rr], c2, mneg));
-        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[rr + 1], c2, mneg));
-        pk[rr >> 1] = pack2(p0, p1);
+        const float x0 = shifted ? sc[rr] - shift : sc[rr];
+        const float x1 = shifted ? sc[rr + 1] - shift : sc[rr + 1];
+        pk[rr >> 1] = pack2(__builtin_amdgcn_exp2f(x0), __builtin_amdgcn_exp2f(x1));
         if (rr & 2) ls1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[rr >> 1]), one2, ls1, false);
         else        ls0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[rr >> 1]), one2, ls0, false);
       }
       ls = ls0 + ls1;
     };
-    probs();
-    if (__any(!(ls <= kSumLimit))) {   // the max grew (or first chunk): rescale, redo
+    probs(0.f, false);
+    // Redo when a lane sum overflows the bound (the max grew) or the lane has
+    // no max yet: take the chunk's max, rescale O and l, recompute P.
+    if (__any(!(ls <= kSumLimit) || m_run < -1e29f)) {
       float mx = sc[0];
 #pragma unroll
       for (int rr = 1; rr < 16; ++rr) mx = fmaxf(mx, sc[rr]);
-      mx = swap_max(mx) * c2;
-      if (mx > m_run) {
-        const float alpha = __builtin_amdgcn_exp2f(m_run - mx);
-        m_run = mx;
+      const float mb = m_run > -1e29f ? m_run : 0.f;   // the offset in sc
+      const float mabs = mb + swap_max(mx);
+      if (mabs > m_run) {
+        const float alpha = __builtin_amdgcn_exp2f(m_run - mabs);   // 0 while unset
+        m_run = mabs;
         l_run *= alpha;
 #pragma unroll
         for (int db = 0; db < NDB; ++db) oacc[db] *= alpha;
       }
-      probs();
+      const float mnew = m_run > -1e29f ? m_run : 0.f;
+      probs(mnew - mb, true);
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) negm[rr] = -mnew;
     }
     l_run += ls;
     // O^T[db] += V^T . P^T over 2 key steps of 16 (V^T operands: keys
@@ -528,6 +551,8 @@ k_attn_mfma(AttnArgs a) {
       hi_c = cn.hi;
     }
     step(kt, vt, lo, hi);
+    // The products are issued before the wait, so they run during it.
+    __builtin_amdgcn_sched_barrier(0);
     // Chunk c + 1 has landed (this wave's part) and every wave is past its
     // reads of chunk c before any starts chunk c + 2 into the same buffers.
     __builtin_amdgcn_s_waitcnt(kWaitVm0);
