@@ -20,6 +20,12 @@ Steps, in the paper's order and notation:
                (Section 2.2.1, "Top-k Gating"); ties are broken by keeping the
                lower key-block index.  Also the window gate and the dense gate
                used as controls.
+  shared    -- the head-shared gate variant: S summed over heads in head
+               order, one kept list per (batch, query block) for every head.
+  layers    -- a stack of calls: layer l uses the offset on even l and its
+               negation on odd l (Section 2.2.2), a per-layer keep (the
+               layer-importance-aware sparsity of Table 2) and may be skipped
+               (Section 2.1.2, Sparse-Depth Pruning).
   mask      -- expand G to token resolution, pad text rows and columns with
                ones (Section 2.2.1; Algorithm 1, expand and pad steps).
   attention -- masked softmax attention over [text; image] in fp64
@@ -41,7 +47,7 @@ from typing import Iterable, Optional, Sequence
 
 import numpy as np
 
-GATES = ("topk", "window", "dense")
+GATES = ("topk", "window", "dense", "topk_shared")
 
 
 # --------------------------------------------------------------------------
@@ -91,6 +97,17 @@ def affinity(qb: np.ndarray, kb: np.ndarray) -> np.ndarray:
     """
     prod = qb[..., :, None, :] * kb[..., None, :, :]               # [..., T_b, T_b, C]
     return np.add.accumulate(prod, axis=-1)[..., -1]
+
+
+def shared_affinity(s: np.ndarray) -> np.ndarray:
+    """Head-shared affinity: S[b] = sum over heads h of S[b, h], added in head
+    order 0, 1, ..., H-1 in fp64.  ``s[B, H, T_b, T_b]`` -> ``[B, T_b, T_b]``.
+
+    The paper's gate is stated per attention call with C channels (Section
+    2.2.1); one gate shared by all heads is the variant whose score is the sum
+    of the per-head scores.
+    """
+    return np.add.accumulate(np.asarray(s, np.float64), axis=1)[:, -1]
 
 
 # --------------------------------------------------------------------------
@@ -161,6 +178,16 @@ def build_index(q: np.ndarray, k: np.ndarray, *, grid_h: int, grid_w: int, tile:
         lists = [[[gate_topk_row(s[b, h, i], keep) for i in range(n_tiles)]
                   for h in range(h_n)] for b in range(b_n)]
         parts = {"qb": qb, "kb": kb, "S": s, "tiles": tiles}
+    elif gate == "topk_shared":
+        if not 1 <= keep <= n_tiles:
+            raise ValueError("keep must be in [1, T_b]")
+        qb = pool_sums(q[:, :, n_text:, :], tiles)
+        kb = pool_sums(k[:, :, n_text:, :], tiles)
+        s = affinity(qb, kb)
+        s_shared = shared_affinity(s)
+        rows = [[gate_topk_row(s_shared[b, i], keep) for i in range(n_tiles)] for b in range(b_n)]
+        lists = [[rows[b] for _ in range(h_n)] for b in range(b_n)]
+        parts = {"qb": qb, "kb": kb, "S": s, "S_shared": s_shared, "tiles": tiles}
     elif gate == "window":
         wl = gate_window(ny, nx, window[0], window[1])
         lists = [[wl for _ in range(h_n)] for _ in range(b_n)]
@@ -254,3 +281,27 @@ def layer_shift(layer: int, tile: int):
     layers (Section 2.2.2, with Bt/2 = 4 for the paper's 8x8 blocks)."""
     h = tile // 2
     return (h, h) if layer % 2 == 0 else (-h, -h)
+
+
+def ssba_layers(layers, *, grid_h, grid_w, tile, shift=None, n_text=0, gate="topk",
+                window=(1, 1), scale=None):
+    """A stack of SSBA calls, one per layer (Section 2.2.2 alternation; the
+    per-layer sparsity of the layer-importance-aware scheme; skipped layers of
+    the depth-pruned model).
+
+    ``layers``: sequence of dicts with ``q``, ``k``, ``v`` ([B, H, T, C]),
+    ``keep`` (top-k gates) and optional ``skip``.  Layer l uses ``shift`` on
+    even l and its negation on odd l (default: (Bt/2, Bt/2), the paper's
+    rule).  Returns per layer (index, output), or None for a skipped layer.
+    """
+    base = (tile // 2, tile // 2) if shift is None else tuple(shift)
+    out = []
+    for l, layer in enumerate(layers):
+        if layer.get("skip", False):
+            out.append(None)
+            continue
+        sh = base if l % 2 == 0 else (-base[0], -base[1])
+        out.append(ssba(layer["q"], layer["k"], layer["v"], grid_h=grid_h, grid_w=grid_w,
+                        tile=tile, shift=sh, n_text=n_text, gate=gate,
+                        keep=layer.get("keep", 0), window=window, scale=scale))
+    return out

@@ -143,3 +143,86 @@ def test_index_layout_dense_and_window():
     assert idx[0, 0, 3].tolist() == [2, 2, 3, -1, -1]
     with pytest.raises(ValueError):
         O.build_index(q, q, grid_h=8, grid_w=8, tile=4, gate="topk", keep=0)
+
+
+# --------------------------------------------------------------------------
+# Head-shared gate (the gate variant whose score is the sum over heads of the
+# per-head affinities) and the layer stack (Section 2.2.2 alternation).
+# --------------------------------------------------------------------------
+def _int_bruteforce_shared(q, k, grid, tile, shift, keep, n_text=0):
+    """Pure-integer reference: pooled sums, products and sums are exact, so
+    any order gives the same S; kept lists by sorting (-S, j)."""
+    b_n, h_n, _, c_n = q.shape
+    tmap = _tile_map(grid, tile, shift[0], shift[1])
+    tb = (grid // tile) ** 2
+    out = []
+    for b in range(b_n):
+        s = [[0] * tb for _ in range(tb)]
+        for h in range(h_n):
+            qb = [[0] * c_n for _ in range(tb)]
+            kb = [[0] * c_n for _ in range(tb)]
+            for tok in range(grid * grid):
+                t = int(tmap[tok])
+                for c in range(c_n):
+                    qb[t][c] += int(q[b, h, n_text + tok, c])
+                    kb[t][c] += int(k[b, h, n_text + tok, c])
+            for i in range(tb):
+                for j in range(tb):
+                    s[i][j] += sum(qb[i][c] * kb[j][c] for c in range(c_n))
+        out.append([sorted(sorted(range(tb), key=lambda j: (-s[i][j], j))[:keep]) for i in range(tb)])
+    return out
+
+
+@pytest.mark.parametrize("shift,keep,n_text", [((2, 2), 4, 0), ((-2, -2), 5, 3), ((1, 3), 1, 0)])
+def test_shared_gate_integer_bruteforce(shift, keep, n_text):
+    grid, tile = 8, 2
+    rng = np.random.default_rng(keep * 7 + n_text)
+    q = rng.integers(-3, 4, size=(2, 3, n_text + grid * grid, 4)).astype(np.float64)
+    k = rng.integers(-3, 4, size=(2, 3, n_text + grid * grid, 4)).astype(np.float64)
+    idx = O.build_index(q, k, grid_h=grid, grid_w=grid, tile=tile, shift=shift, n_text=n_text,
+                        gate="topk_shared", keep=keep)
+    ref = _int_bruteforce_shared(q, k, grid, tile, shift, keep, n_text)
+    for b in range(2):
+        for h in range(3):
+            for i in range(16):
+                assert idx[b, h, i, 0] == keep
+                assert idx[b, h, i, 1:1 + keep].tolist() == ref[b][i]
+                assert (idx[b, h, i, 1 + keep:] == -1).all()
+
+
+def test_shared_gate_one_head_equals_per_head_gate():
+    rng = np.random.default_rng(3)
+    q = rng.standard_normal((2, 1, 256, 8))
+    k = rng.standard_normal((2, 1, 256, 8))
+    kw = dict(grid_h=16, grid_w=16, tile=4, shift=(2, 2), keep=5)
+    assert (O.build_index(q, k, gate="topk_shared", **kw) == O.build_index(q, k, gate="topk", **kw)).all()
+
+
+def test_shared_affinity_adds_heads_in_order():
+    """Three heads whose per-head scores are 1, 2^-53 and 2^-53: left to
+    right the two tiny terms each round away (1 + 2^-53 = 1 in fp64, ties to
+    even); any other order would keep them (2^-52 + 1 is exact)."""
+    s = np.zeros((1, 3, 1, 1))
+    s[0, :, 0, 0] = [1.0, 2.0 ** -53, 2.0 ** -53]
+    assert O.shared_affinity(s)[0, 0, 0] == 1.0
+
+
+def test_layer_stack_alternates_shift_and_skips():
+    grid, tile = 16, 4
+    rng = np.random.default_rng(9)
+    mk = lambda: rng.standard_normal((1, 2, grid * grid, 8))
+    layers = [dict(q=mk(), k=mk(), v=mk(), keep=k) for k in (3, 6, 2)]
+    layers[1]["skip"] = True
+    res = O.ssba_layers(layers, grid_h=grid, grid_w=grid, tile=tile)
+    assert res[1] is None
+    for l in (0, 2):
+        sh = O.layer_shift(l, tile)
+        ref = O.ssba(layers[l]["q"], layers[l]["k"], layers[l]["v"], grid_h=grid, grid_w=grid,
+                     tile=tile, shift=sh, keep=layers[l]["keep"])
+        assert (res[l][0] == ref[0]).all() and np.array_equal(res[l][1], ref[1])
+    # an odd layer takes the negated offset: (-2, -2) here
+    layers[1]["skip"] = False
+    res = O.ssba_layers(layers, grid_h=grid, grid_w=grid, tile=tile)
+    ref = O.build_index(layers[1]["q"], layers[1]["k"], grid_h=grid, grid_w=grid, tile=tile,
+                        shift=(-2, -2), keep=6)
+    assert (res[1][0] == ref).all()
