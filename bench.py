@@ -1,7 +1,7 @@
 """Benchmark of the SSBA forward path on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload grid64]
-                    [--no-cpu] [--sweep] [--copy-calibration]
+                    [--no-cpu] [--sweep] [--copy-calibration] [--layers]
 
 One step = one SSBA layer call on inputs already resident in HBM: the top-k
 gate (block pooling, affinity, ranking -> index) and the block-sparse
@@ -31,6 +31,12 @@ it runs on).  `traffic` is the HBM traffic per launch measured with rocprofv3
 counters (FETCH_SIZE and WRITE_SIZE, scaled by what the same counters read
 for a plain copy of known size), reported only while the kernel's sources
 still hash to the values the counters were taken on.
+
+--layers prints instead one JSON line for a 24-layer stack through
+ssba_forward_layers (synthetic per-layer keep schedule averaging 84.18 %
+masked, the offset alternating with layer parity, distinct inputs per layer):
+the stack, the same layers as separate calls, a depth-pruned stack, the
+head-shared gate and the window gate with its per-parity index cache.
 
 --copy-calibration runs only that plain copy (256 MiB, 5 times) for the
 counter runs and prints its size.
@@ -284,6 +290,85 @@ def measure(w, steps: int, warmup: int, dense_steps: int, graph: bool = True):
     }
 
 
+def measure_layers(w, steps: int, warmup: int) -> dict:
+    """A 24-layer stack through ssba_forward_layers: the synthetic per-layer
+    keep schedule, the offset alternating by layer parity, every layer with
+    its own seeded Q, K, V (so the stack's 768 MB do not fit the MALL)."""
+    import torch
+    from paper_2605_15684_amd import ssba
+    from paper_2605_15684_amd.inputs import LAYER_KEEP_SCHEDULE_24, LAYER_SKIP_24, make_qkv
+    keeps = LAYER_KEEP_SCHEDULE_24
+    layers = []
+    for l, kp in enumerate(keeps):
+        q, k, v = make_qkv(w.with_(seed=w.seed + 100 + l), device="cuda")
+        layers.append(dict(q=q, k=k, v=v, out=torch.empty_like(q), keep=kp))
+    desc = ssba.desc_for(layers[0]["q"], grid=(w.grid_h, w.grid_w), tile=w.tile, shift=w.shift,
+                         n_text=w.n_text, gate="topk", keep=keeps[0])
+
+    def span(fn, n):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    index, scratch = ssba.forward_layers(layers, desc)
+    ms_stack = span(lambda: ssba.forward_layers(layers, desc, index, scratch), steps)
+
+    # The same layers as 24 separate fused calls from Python.
+    per = []
+    for l, L in enumerate(layers):
+        dl = ssba.desc_for(L["q"], grid=(w.grid_h, w.grid_w), tile=w.tile,
+                           shift=ssba.layer_shift(l, w.tile), n_text=w.n_text, gate="topk", keep=keeps[l])
+        il, sl = ssba.alloc_workspace(dl, L["q"].device)
+        per.append((L, dl, il, sl))
+
+    def separate():
+        for L, dl, il, sl in per:
+            ssba.forward_topk(L["q"], L["k"], L["v"], dl, il, sl, L["out"])
+    ms_separate = span(separate, steps)
+
+    # Depth-pruned stack: the skip mask of the bench (6 of 24 layers skipped).
+    pruned = [dict(L, skip=sk) for L, sk in zip(layers, LAYER_SKIP_24)]
+    ms_pruned = span(lambda: ssba.forward_layers(pruned, desc, index, scratch), steps)
+
+    # Head-shared gate on the same stack.
+    d_sh = ssba.desc_for(layers[0]["q"], grid=(w.grid_h, w.grid_w), tile=w.tile, shift=w.shift,
+                         n_text=w.n_text, gate="topk_shared", keep=keeps[0])
+    i_sh, s_sh = ssba.forward_layers(layers, d_sh)
+    ms_shared = span(lambda: ssba.forward_layers(layers, d_sh, i_sh, s_sh), steps)
+
+    # Window gate (4x4 blocks, 75 % masked): the index is built once per parity.
+    d_win = ssba.desc_for(layers[0]["q"], grid=(w.grid_h, w.grid_w), tile=w.tile, shift=w.shift,
+                          n_text=w.n_text, gate="window", window=(4, 4))
+    i_w, s_w = ssba.forward_layers(layers, d_win)
+    ms_window = span(lambda: ssba.forward_layers(layers, d_win, i_w, s_w), steps)
+
+    gf = sum(flops(w.with_(keep=kp)) for kp in keeps)
+    gf_pruned = sum(flops(w.with_(keep=kp)) for kp, sk in zip(keeps, LAYER_SKIP_24) if not sk)
+    masked = 1.0 - sum(keeps) / (len(keeps) * w.n_tiles)
+    return {
+        "metric": "SSBA 24-layer stack ms/call + effective TFLOP/s (per-layer keep schedule, "
+                  f"{100 * masked:.2f}% average masked, offsets alternating)",
+        "value": round(gf / (ms_stack * 1e-3) / 1e12, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": steps, "warmup": warmup, "ms_per_step": round(ms_stack, 5), "higher_is_better": True,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{w.name} x 24 layers: {describe(w)} (keep per layer {list(keeps)})"},
+        "ms_per_layer": round(ms_stack / len(keeps), 5),
+        "ms_separate_fused_calls": round(ms_separate, 5),
+        "ms_pruned_stack": round(ms_pruned, 5), "pruned_layers_skipped": int(sum(LAYER_SKIP_24)),
+        "tflops_pruned": round(gf_pruned / (ms_pruned * 1e-3) / 1e12, 2),
+        "ms_shared_gate_stack": round(ms_shared, 5),
+        "ms_window_stack": round(ms_window, 5),
+        "gflop_stack": round(gf / 1e9, 3),
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -293,6 +378,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--layers", action="store_true",
+                    help="measure the 24-layer stack (ssba_forward_layers) instead of one call")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the SSBA path has no multi-GPU mode in this build "
@@ -312,6 +399,9 @@ def main():
         return
 
     w = preset(args.workload)
+    if args.layers:
+        print(json.dumps(measure_layers(w, max(5, args.steps // 10), max(2, args.warmup // 10))), flush=True)
+        return
     r, m = measure(w, args.steps, args.warmup, max(20, args.steps // 4))
     f = flops(w)
     achieved = f / (m["ms_fwd"] * 1e-3) / 1e12

@@ -9,7 +9,7 @@
  * block keeps a subset of image key blocks (the gate).  Text tokens see
  * everything and are seen by everything (Algorithm 1, pad step).
  *
- * Gates (all three emit the same index layout, consumed by ssba_forward):
+ * Gates (all four emit the same index layout, consumed by ssba_forward):
  *   SSBA_GATE_TOPK   -- Section 2.2.1 "Block Compression", "Affinity Matrix",
  *                       "Top-k Gating" (Eq. 1; Algorithm 1, pool/affinity/
  *                       top-k steps): per-block pooled Q and K, S = q_b k_b^T,
@@ -20,6 +20,12 @@
  *                       in slot order; S is summed over channels in order,
  *                       without fused multiply-add.  Lists are therefore
  *                       bit-reproducible.
+ *   SSBA_GATE_TOPK_SHARED -- the top-k gate with one score shared by all heads
+ *                       of a batch element: S = sum over heads of the per-head
+ *                       S_h (each as for TOPK), added in head order 0..H-1 in
+ *                       fp64; every head receives the same kept lists.  The
+ *                       paper states one gate per attention call over its
+ *                       channels (Section 2.2.1); this is the shared variant.
  *   SSBA_GATE_WINDOW -- control gate: block i sees block j iff both lie in one
  *                       win_h x win_w window of blocks of the shifted frame.
  *   SSBA_GATE_DENSE  -- every block sees every block (zero sparsity).
@@ -57,7 +63,7 @@
 extern "C" {
 #endif
 
-#define SSBA_ABI_VERSION 1
+#define SSBA_ABI_VERSION 2
 
 typedef enum {
   SSBA_OK = 0,
@@ -70,7 +76,12 @@ typedef enum {
 } ssba_status;
 
 typedef enum { SSBA_DT_BF16 = 0, SSBA_DT_F32 = 1 } ssba_dtype;
-typedef enum { SSBA_GATE_TOPK = 0, SSBA_GATE_WINDOW = 1, SSBA_GATE_DENSE = 2 } ssba_gate;
+typedef enum {
+  SSBA_GATE_TOPK = 0,
+  SSBA_GATE_WINDOW = 1,
+  SSBA_GATE_DENSE = 2,
+  SSBA_GATE_TOPK_SHARED = 3
+} ssba_gate;
 
 typedef struct ssba_desc {
   int32_t batch, heads, head_dim;  /* B >= 1, H >= 1, D in {64, 128}               */
@@ -78,7 +89,7 @@ typedef struct ssba_desc {
   int32_t shift_y, shift_x;        /* Delta, any sign, reduced mod the grid          */
   int32_t n_text;                  /* >= 0 text tokens, stored before the image rows */
   int32_t gate;                    /* ssba_gate                                      */
-  int32_t keep;                    /* TOPK: kept key blocks per query block, 1..T_b  */
+  int32_t keep;                    /* TOPK, TOPK_SHARED: kept key blocks per query block, 1..T_b */
   int32_t win_h, win_w;            /* WINDOW: window in blocks; n_y % win_h == n_x % win_w == 0 */
   int32_t dtype;                   /* ssba_dtype of Q, K, V and O                    */
   float softmax_scale;             /* <= 0 selects 1 / sqrt(head_dim)                */
@@ -95,6 +106,8 @@ const char* ssba_status_str(ssba_status s);
  *   index_bytes   = 4 * B * H * T_b * (1 + T_b): the index of ssba_build_index.
  *   scratch_bytes = TOPK: 16 * B * H * T_b * D (fp64 pooled q_b and k_b)
  *                   + 4 * B * H * T_b (per-row status flags);
+ *                   TOPK_SHARED: as TOPK + 8 * B * H * T_b^2 (fp64 per-head
+ *                   affinity rows);
  *                   WINDOW / DENSE: 4 * B * H * T_b.
  * Either output pointer may be NULL.  T_b = grid_h * grid_w / Bt^2. */
 ssba_status ssba_workspace_size(const ssba_desc* d, size_t* index_bytes, size_t* scratch_bytes);
@@ -102,8 +115,9 @@ ssba_status ssba_workspace_size(const ssba_desc* d, size_t* index_bytes, size_t*
 /* Gate (Section 2.2.1 Block Compression / Affinity / Top-k Gating; Algorithm 1
  * pool, affinity, top-k and expand steps).  Writes `index`, int32
  * [B][H][T_b][1 + T_b]: entry 0 = count of kept key blocks, then their block
- * ids ascending, then -1 padding.  TOPK reads the image rows of q and k (dtype
- * d->dtype, layout above); WINDOW and DENSE read neither (q, k may be NULL).
+ * ids ascending, then -1 padding.  TOPK and TOPK_SHARED read the image rows of
+ * q and k (dtype d->dtype, layout above); WINDOW and DENSE read neither (q, k
+ * may be NULL).
  * `scratch` (scratch_bytes, 16-byte aligned) is overwritten; its status
  * flags are read by ssba_read_device_status. */
 ssba_status ssba_build_index(const ssba_desc* d, const void* q, const void* k,
@@ -131,14 +145,49 @@ ssba_status ssba_forward_dense(const ssba_desc* d, const void* q, const void* k,
  * kernel, Section 2.2.1 and Algorithm 1 pool through attend steps): the same
  * results as ssba_build_index followed by ssba_forward -- `index` receives
  * bit-identical index rows, `scratch` the same status flags, `o` the same
- * output -- with one pass fewer over Q.  d->gate must be SSBA_GATE_TOPK.
- * For bf16 inputs with 8x8 blocks, head_dim 64 or 128 and at most 64 blocks
- * it launches a pooling kernel for K only and an attention kernel in which
- * each query block pools its own queries, forms its affinity row and ranks
- * it before attending; other shapes run the two calls.  Buffers, sizes and
- * alignment as for ssba_build_index and ssba_forward. */
+ * output -- with one launch fewer.  d->gate must be SSBA_GATE_TOPK or
+ * SSBA_GATE_TOPK_SHARED.  For TOPK with bf16 inputs, 8x8 blocks, head_dim 64
+ * or 128 and at most 64 blocks it launches the pooling kernel and an
+ * attention kernel in which each query block forms its affinity row from the
+ * pooled sums and ranks it before attending; other shapes and the shared
+ * gate run the two calls.  Buffers, sizes and alignment as for
+ * ssba_build_index and ssba_forward. */
 ssba_status ssba_forward_topk(const ssba_desc* d, const void* q, const void* k, const void* v,
                               int32_t* index, void* scratch, void* o, void* hip_stream);
+
+/* One layer of a stack run by ssba_forward_layers. */
+typedef struct ssba_layer {
+  const void* q;    /* this layer's Q, K, V and output O (layout of the descriptor) */
+  const void* k;
+  const void* v;
+  void* o;
+  int32_t keep;     /* top-k gates: kept key blocks per query block, 1..T_b      */
+  int32_t skip;     /* nonzero: the layer is skipped (nothing runs, o untouched)  */
+} ssba_layer;
+
+/* Device bytes ssba_forward_layers needs for n_layers layers of descriptor d
+ * (d->keep is not used): index_bytes = n_layers * the index of one call;
+ * scratch_bytes = n_layers * the scratch of one call rounded up to 256 bytes.
+ * Layer l's slices start at l * (index_bytes / n_layers) and
+ * l * (scratch_bytes / n_layers). */
+ssba_status ssba_layers_workspace_size(const ssba_desc* d, int n_layers, size_t* index_bytes,
+                                       size_t* scratch_bytes);
+
+/* A stack of SSBA layer calls on one stream (Section 2.2.2 offset alternation;
+ * the per-layer sparsity of the layer-importance-aware scheme, Table 2; the
+ * skipped blocks of Sparse-Depth Pruning, Section 2.1.2).  Layer l uses the
+ * offset (d->shift_y, d->shift_x) on even l and its negation on odd l (the
+ * paper's rule with (Bt/2, Bt/2)), layers[l].keep for the top-k gates, and
+ * does nothing if layers[l].skip.  Each layer's results equal one
+ * ssba_forward_topk call (top-k gates) or ssba_build_index + ssba_forward
+ * (static gates) with that layer's descriptor, index slice and scratch slice.
+ * Static gates depend only on the frame, so the index is built once per
+ * offset parity (in the slice of the first layer of that parity that runs)
+ * and reused by the later layers of that parity, whose slices are left
+ * untouched.  Every layer is checked before anything is launched; a HIP
+ * launch failure stops the stack after the layers already enqueued. */
+ssba_status ssba_forward_layers(const ssba_desc* d, const ssba_layer* layers, int n_layers,
+                                int32_t* index, void* scratch, void* hip_stream);
 
 /* Name of the attention kernel that ssba_forward (mode 0), ssba_forward_dense
  * (mode 1) or ssba_forward_topk (mode 2) launches for this descriptor, as
@@ -149,7 +198,8 @@ const char* ssba_forward_kernel(const ssba_desc* d, int mode);
 
 /* Synchronizes `hip_stream`, then reads the status flags that the last
  * ssba_build_index left in `scratch` (same descriptor): SSBA_OK, or
- * SSBA_ERR_NONFINITE if any affinity row held a NaN or Inf (TOPK only). */
+ * SSBA_ERR_NONFINITE if any affinity row held a NaN or Inf (top-k gates only;
+ * for the shared gate, the summed row).  d->keep is not used here. */
 ssba_status ssba_read_device_status(const ssba_desc* d, const void* scratch, ssba_status* out,
                                     void* hip_stream);
 

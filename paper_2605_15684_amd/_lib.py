@@ -24,10 +24,12 @@ DT_F32 = 1
 GATE_TOPK = 0
 GATE_WINDOW = 1
 GATE_DENSE = 2
+GATE_TOPK_SHARED = 3
 
 EXPORTS = ("ssba_abi_version", "ssba_status_str", "ssba_workspace_size", "ssba_build_index",
            "ssba_forward", "ssba_forward_dense", "ssba_read_device_status",
-           "ssba_forward_kernel", "ssba_forward_topk")
+           "ssba_forward_kernel", "ssba_forward_topk", "ssba_layers_workspace_size",
+           "ssba_forward_layers")
 
 
 class SsbaDesc(ctypes.Structure):
@@ -40,6 +42,11 @@ class SsbaDesc(ctypes.Structure):
         ("softmax_scale", ctypes.c_float),
         ("stride_b", ctypes.c_int64), ("stride_h", ctypes.c_int64), ("stride_t", ctypes.c_int64),
     ]
+
+
+class SsbaLayer(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_void_p), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
+                ("o", ctypes.c_void_p), ("keep", ctypes.c_int32), ("skip", ctypes.c_int32)]
 
 
 class SsbaError(RuntimeError):
@@ -87,6 +94,10 @@ def load(path: str = None) -> ctypes.CDLL:
     lib.ssba_forward_topk.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp]
     lib.ssba_forward_kernel.restype = ctypes.c_char_p
     lib.ssba_forward_kernel.argtypes = [dp, ctypes.c_int]
+    lib.ssba_layers_workspace_size.restype = ctypes.c_int
+    lib.ssba_layers_workspace_size.argtypes = [dp, ctypes.c_int, ctypes.POINTER(sz), ctypes.POINTER(sz)]
+    lib.ssba_forward_layers.restype = ctypes.c_int
+    lib.ssba_forward_layers.argtypes = [dp, ctypes.POINTER(SsbaLayer), ctypes.c_int, vp, vp, vp]
     lib.ssba_read_device_status.restype = ctypes.c_int
     lib.ssba_read_device_status.argtypes = [dp, vp, ctypes.POINTER(ctypes.c_int), vp]
     _lib = lib
@@ -139,3 +150,16 @@ def forward_kernel(desc, dense: bool = False, mode: int = None):
     m = (1 if dense else 0) if mode is None else mode
     name = load().ssba_forward_kernel(ctypes.byref(desc), m)
     return None if name is None else name.decode()
+
+
+def layers_workspace_size(desc: SsbaDesc, n_layers: int):
+    ib, sb = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    check(load().ssba_layers_workspace_size(ctypes.byref(desc), int(n_layers), ctypes.byref(ib),
+                                            ctypes.byref(sb)), "ssba_layers_workspace_size")
+    return ib.value, sb.value
+
+
+def forward_layers(desc, layers, index_ptr, scratch_ptr, stream) -> int:
+    """`layers`: a ctypes array of SsbaLayer."""
+    return load().ssba_forward_layers(ctypes.byref(desc), layers, len(layers), index_ptr, scratch_ptr,
+                                      stream)

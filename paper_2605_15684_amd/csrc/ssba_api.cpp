@@ -17,6 +17,8 @@ using ssba::IndexArgs;
 
 constexpr int kMaxTiles = 1024;  // one gate workgroup ranks a whole row
 
+bool is_topk(int gate) { return gate == SSBA_GATE_TOPK || gate == SSBA_GATE_TOPK_SHARED; }
+
 int ilog2(int v) {
   int l = 0;
   while ((1 << l) < v) ++l;
@@ -42,7 +44,7 @@ ssba_status check_desc(const ssba_desc* d, Shape* out, bool gate_fields = true) 
     return SSBA_ERR_SHAPE;
   if (d->dtype != SSBA_DT_BF16 && d->dtype != SSBA_DT_F32) return SSBA_ERR_ARG;
   if (gate_fields && d->gate != SSBA_GATE_TOPK && d->gate != SSBA_GATE_WINDOW &&
-      d->gate != SSBA_GATE_DENSE)
+      d->gate != SSBA_GATE_DENSE && d->gate != SSBA_GATE_TOPK_SHARED)
     return SSBA_ERR_ARG;
   if (d->head_dim != 64 && d->head_dim != 128) return SSBA_ERR_UNSUPPORTED;
   if (d->tile != 4 && d->tile != 8 && d->tile != 16) return SSBA_ERR_UNSUPPORTED;
@@ -54,8 +56,7 @@ ssba_status check_desc(const ssba_desc* d, Shape* out, bool gate_fields = true) 
   const int64_t n_tiles = t_img / ((int64_t)d->tile * d->tile);
   if (n_tiles > kMaxTiles) return SSBA_ERR_UNSUPPORTED;
   const int ny = d->grid_h / d->tile, nx = d->grid_w / d->tile;
-  if (gate_fields && d->gate == SSBA_GATE_TOPK && (d->keep < 1 || d->keep > n_tiles))
-    return SSBA_ERR_ARG;
+  if (gate_fields && is_topk(d->gate) && (d->keep < 1 || d->keep > n_tiles)) return SSBA_ERR_ARG;
   if (gate_fields && d->gate == SSBA_GATE_WINDOW &&
       (d->win_h < 1 || d->win_w < 1 || ny % d->win_h || nx % d->win_w))
     return SSBA_ERR_ARG;
@@ -97,11 +98,23 @@ size_t index_bytes_of(const ssba_desc* d, const Shape& s) {
   return (size_t)4 * d->batch * d->heads * s.n_tiles * (s.n_tiles + 1);
 }
 
+// Scratch layout: [pooled q_b | pooled k_b] (top-k gates), [per-head
+// affinity rows] (head-shared gate), then the status flags.
+size_t flags_offset_of(const ssba_desc* d, const Shape& s) {
+  const size_t rows = (size_t)d->batch * d->heads * s.n_tiles;
+  size_t off = 0;
+  if (is_topk(d->gate)) off += (size_t)16 * rows * d->head_dim;
+  if (d->gate == SSBA_GATE_TOPK_SHARED) off += (size_t)8 * rows * s.n_tiles;
+  return off;
+}
+
 size_t scratch_bytes_of(const ssba_desc* d, const Shape& s) {
-  const size_t flags = (size_t)4 * d->batch * d->heads * s.n_tiles;
-  if (d->gate == SSBA_GATE_TOPK)
-    return (size_t)16 * d->batch * d->heads * s.n_tiles * d->head_dim + flags;
-  return flags;
+  return flags_offset_of(d, s) + (size_t)4 * d->batch * d->heads * s.n_tiles;
+}
+
+// Per-layer scratch slices of the layer driver start 256-byte aligned.
+size_t layer_scratch_stride(const ssba_desc* d, const Shape& s) {
+  return (scratch_bytes_of(d, s) + 255) / 256 * 256;
 }
 
 AttnArgs attn_args(const ssba_desc* d, const Shape& s, const void* q, const void* k, const void* v,
@@ -177,7 +190,7 @@ ssba_status ssba_workspace_size(const ssba_desc* d, size_t* index_bytes, size_t*
 namespace {
 
 IndexArgs index_args(const ssba_desc* d, const Shape& s, const void* q, const void* k, int32_t* index,
-                     void* scratch, bool topk) {
+                     void* scratch) {
   IndexArgs a;
   std::memset(&a, 0, sizeof(a));
   a.q = q;
@@ -185,9 +198,12 @@ IndexArgs index_args(const ssba_desc* d, const Shape& s, const void* q, const vo
   a.index = index;
   const size_t pooled = (size_t)d->batch * d->heads * s.n_tiles * d->head_dim;
   double* base = static_cast<double*>(scratch);
-  a.qb = topk ? base : nullptr;
-  a.kb = topk ? base + pooled : nullptr;
-  a.flags = reinterpret_cast<int32_t*>(topk ? base + 2 * pooled : base);
+  if (is_topk(d->gate)) {
+    a.qb = base;
+    a.kb = base + pooled;
+  }
+  if (d->gate == SSBA_GATE_TOPK_SHARED) a.srows = base + 2 * pooled;
+  a.flags = reinterpret_cast<int32_t*>(static_cast<char*>(scratch) + flags_offset_of(d, s));
   a.sb = s.sb;
   a.sh = s.sh;
   a.st = s.st;
@@ -219,17 +235,18 @@ ssba_status ssba_build_index(const ssba_desc* d, const void* q, const void* k, i
   const ssba_status st = check_desc(d, &s);
   if (st != SSBA_OK) return st;
   if (!index || !scratch || !aligned(index, 4) || !aligned(scratch, 16)) return SSBA_ERR_ARG;
-  const bool topk = d->gate == SSBA_GATE_TOPK;
+  const bool topk = is_topk(d->gate);
   if (topk) {
     const size_t al = d->dtype == SSBA_DT_BF16 ? 16 : 4;
     if (!q || !k || !aligned(q, al) || !aligned(k, al)) return SSBA_ERR_ARG;
   }
-  const IndexArgs a = index_args(d, s, q, k, index, scratch, topk);
+  const IndexArgs a = index_args(d, s, q, k, index, scratch);
   hipStream_t hs = static_cast<hipStream_t>(stream);
   hipError_t e;
   if (topk) {
     e = ssba::launch_pool(a, d->dtype, hs);
-    if (e == hipSuccess) e = ssba::launch_gate_topk(a, hs);
+    if (e == hipSuccess)
+      e = d->gate == SSBA_GATE_TOPK ? ssba::launch_gate_topk(a, hs) : ssba::launch_gate_topk_shared(a, hs);
   } else {
     e = ssba::launch_gate_static(a, d->gate, hs);
   }
@@ -241,17 +258,17 @@ ssba_status ssba_forward_topk(const ssba_desc* d, const void* q, const void* k, 
   Shape s;
   ssba_status st = check_desc(d, &s);
   if (st != SSBA_OK) return st;
-  if (d->gate != SSBA_GATE_TOPK) return SSBA_ERR_ARG;
+  if (!is_topk(d->gate)) return SSBA_ERR_ARG;
   if (!q || !k || !v || !o || !index || !scratch) return SSBA_ERR_ARG;
   const size_t al = d->dtype == SSBA_DT_BF16 ? 16 : 4;
   if (!aligned(q, al) || !aligned(k, al) || !aligned(v, al) || !aligned(o, al) || !aligned(index, 4) ||
       !aligned(scratch, 16))
     return SSBA_ERR_ARG;
-  if (!gated_supported(d, s)) {   // the two calls, same results
+  if (d->gate != SSBA_GATE_TOPK || !gated_supported(d, s)) {   // the two calls, same results
     st = ssba_build_index(d, q, k, index, scratch, stream);
     return st != SSBA_OK ? st : ssba_forward(d, q, k, v, index, o, stream);
   }
-  IndexArgs ia = index_args(d, s, q, k, index, scratch, true);
+  IndexArgs ia = index_args(d, s, q, k, index, scratch);
   AttnArgs aa = attn_args(d, s, q, k, v, nullptr, o, false);
   aa.gated = 1;
   aa.keep = d->keep;
@@ -269,9 +286,9 @@ const char* ssba_forward_kernel(const ssba_desc* d, int mode) {
   Shape s;
   const bool dense = mode == 1;
   if (mode < 0 || mode > 2 || check_desc(d, &s, !dense) != SSBA_OK) return nullptr;
-  if (mode == 2 && d->gate != SSBA_GATE_TOPK) return nullptr;
+  if (mode == 2 && !is_topk(d->gate)) return nullptr;
   AttnArgs a = attn_args(d, s, nullptr, nullptr, nullptr, nullptr, nullptr, dense);
-  a.gated = (mode == 2 && gated_supported(d, s)) ? 1 : 0;
+  a.gated = (mode == 2 && d->gate == SSBA_GATE_TOPK && gated_supported(d, s)) ? 1 : 0;
   return ssba::attn_kernel_name(a, d->head_dim, d->tile, d->dtype);
 }
 
@@ -285,15 +302,80 @@ ssba_status ssba_forward_dense(const ssba_desc* d, const void* q, const void* k,
   return run_attention(d, q, k, v, nullptr, o, stream, true);
 }
 
+ssba_status ssba_layers_workspace_size(const ssba_desc* d, int n_layers, size_t* index_bytes,
+                                       size_t* scratch_bytes) {
+  if (!d || n_layers < 1) return SSBA_ERR_ARG;
+  ssba_desc base = *d;
+  if (is_topk(base.gate)) base.keep = 1;   // per-layer keeps are checked by the driver
+  Shape s;
+  const ssba_status st = check_desc(&base, &s);
+  if (st != SSBA_OK) return st;
+  if (index_bytes) *index_bytes = (size_t)n_layers * index_bytes_of(&base, s);
+  if (scratch_bytes) *scratch_bytes = (size_t)n_layers * layer_scratch_stride(&base, s);
+  return SSBA_OK;
+}
+
+ssba_status ssba_forward_layers(const ssba_desc* d, const ssba_layer* layers, int n_layers,
+                                int32_t* index, void* scratch, void* stream) {
+  if (!d || !layers || n_layers < 1) return SSBA_ERR_ARG;
+  ssba_desc base = *d;
+  if (is_topk(base.gate)) base.keep = 1;
+  Shape s;
+  ssba_status st = check_desc(&base, &s);
+  if (st != SSBA_OK) return st;
+  if (!index || !scratch || !aligned(index, 4) || !aligned(scratch, 16)) return SSBA_ERR_ARG;
+  // Every layer is checked before the first launch.
+  const size_t al = d->dtype == SSBA_DT_BF16 ? 16 : 4;
+  for (int l = 0; l < n_layers; ++l) {
+    const ssba_layer& L = layers[l];
+    if (L.skip) continue;
+    if (!L.q || !L.k || !L.v || !L.o || !aligned(L.q, al) || !aligned(L.k, al) || !aligned(L.v, al) ||
+        !aligned(L.o, al))
+      return SSBA_ERR_ARG;
+    if (is_topk(d->gate) && (L.keep < 1 || L.keep > s.n_tiles)) return SSBA_ERR_ARG;
+  }
+  const size_t idx_elems = index_bytes_of(&base, s) / sizeof(int32_t);
+  const size_t scr_stride = layer_scratch_stride(&base, s);
+  int cached[2] = {-1, -1};   // static gates: the layer whose index serves each parity
+  for (int l = 0; l < n_layers; ++l) {
+    const ssba_layer& L = layers[l];
+    if (L.skip) continue;
+    ssba_desc dl = base;
+    if (l & 1) {   // Section 2.2.2: the offset alternates sign between layers
+      dl.shift_y = -d->shift_y;
+      dl.shift_x = -d->shift_x;
+    }
+    int32_t* il = index + (size_t)l * idx_elems;
+    void* sl = static_cast<char*>(scratch) + (size_t)l * scr_stride;
+    if (is_topk(d->gate)) {
+      dl.keep = L.keep;
+      st = ssba_forward_topk(&dl, L.q, L.k, L.v, il, sl, L.o, stream);
+    } else {
+      const int par = l & 1;
+      if (cached[par] < 0) {
+        st = ssba_build_index(&dl, nullptr, nullptr, il, sl, stream);
+        if (st != SSBA_OK) return st;
+        cached[par] = l;
+      }
+      st = ssba_forward(&dl, L.q, L.k, L.v, index + (size_t)cached[par] * idx_elems, L.o, stream);
+    }
+    if (st != SSBA_OK) return st;
+  }
+  return SSBA_OK;
+}
+
 ssba_status ssba_read_device_status(const ssba_desc* d, const void* scratch, ssba_status* out,
                                     void* stream) {
+  if (!d) return SSBA_ERR_ARG;
+  ssba_desc base = *d;   // the flags do not depend on keep
+  if (is_topk(base.gate) && base.keep < 1) base.keep = 1;
   Shape s;
-  const ssba_status st = check_desc(d, &s);
+  const ssba_status st = check_desc(&base, &s);
   if (st != SSBA_OK) return st;
   if (!scratch || !out || !aligned(scratch, 8)) return SSBA_ERR_ARG;
   const size_t n = (size_t)d->batch * d->heads * s.n_tiles;
-  const size_t pooled = d->gate == SSBA_GATE_TOPK ? (size_t)16 * n * d->head_dim : 0;
-  const int32_t* flags = reinterpret_cast<const int32_t*>(static_cast<const char*>(scratch) + pooled);
+  const int32_t* flags =
+      reinterpret_cast<const int32_t*>(static_cast<const char*>(scratch) + flags_offset_of(d, s));
   std::vector<int32_t> host(n);
   hipStream_t hs = static_cast<hipStream_t>(stream);
   if (hipMemcpyAsync(host.data(), flags, n * sizeof(int32_t), hipMemcpyDeviceToHost, hs) != hipSuccess)

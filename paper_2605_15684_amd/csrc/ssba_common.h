@@ -101,6 +101,7 @@ struct IndexArgs {
   double* qb;            // [B][H][T_b][D] pooled sums
   double* kb;
   int32_t* flags;        // [B][H][T_b]
+  double* srows;         // [B][H][T_b][T_b] per-head affinity rows (head-shared gate)
   int64_t sb, sh, st;
   int batch, heads, head_dim, n_tiles, keep, win_h, win_w, ny;
   Frame f;
@@ -109,6 +110,8 @@ struct IndexArgs {
 // Launchers (each returns hipGetLastError() of its launch).
 hipError_t launch_pool(const IndexArgs& a, int dtype, hipStream_t s);
 hipError_t launch_gate_topk(const IndexArgs& a, hipStream_t s);
+// Head-shared top-k gate: per-head affinity rows, then their sum over heads.
+hipError_t launch_gate_topk_shared(const IndexArgs& a, hipStream_t s);
 hipError_t launch_gate_static(const IndexArgs& a, int gate, hipStream_t s);
 hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, int tile, hipStream_t s);
 hipError_t launch_attn_f32(const AttnArgs& a, int head_dim, int tile, hipStream_t s);

@@ -108,11 +108,46 @@ __global__ void __launch_bounds__(256) k_pool(IndexArgs a) {
   }
 }
 
+// S[i][j] of one (batch, head): the channel-ordered sum of the rounded
+// products of the pooled query row qr (channel c at qr[c]) and the pooled key
+// column kc (channel c at kc[c * tb]).  Each batch of pooled-k loads is
+// requested before its first product, so a batch costs one memory round trip.
+template <int D>
+__device__ __forceinline__ double affinity_entry(const double* qr, const double* kc, int tb) {
+  constexpr int BATCH = D < 64 ? D : 64;
+  double s = 0.0;
+#pragma unroll
+  for (int c0 = 0; c0 < D; c0 += BATCH) {
+    double kv[BATCH];
+#pragma unroll
+    for (int u = 0; u < BATCH; ++u) kv[u] = kc[(int64_t)(c0 + u) * tb];
+#pragma unroll
+    for (int u = 0; u < BATCH; ++u) {
+      const double p = __dmul_rn(qr[c0 + u], kv[u]);
+      s = (c0 + u == 0) ? p : __dadd_rn(s, p);
+    }
+  }
+  return s;
+}
+
+// Kept flag of block j (thread j of the workgroup) among the tb keys of the
+// row: the `keep` first in (key descending, block id ascending).  MAXT == 64
+// ranks in one wave; larger rows count, per key, the keys ranked before it.
+template <int MAXT>
+__device__ __forceinline__ bool rank_kept(uint64_t key, int j, int tb, int keep, const uint64_t* keys) {
+  if (MAXT == 64) return wave_topk(key, j < tb, keep, j & 63);
+  if (j >= tb) return false;
+  int rank = 0;
+  for (int jj = 0; jj < tb; ++jj) {
+    const uint64_t kj = keys[jj];
+    rank += (kj > key || (kj == key && jj < j)) ? 1 : 0;
+  }
+  return rank < keep;
+}
+
 // One workgroup per query block (i, h, b); thread j computes S[i][j] (the
 // channel-ordered sum of rounded products) and its rank.  The `keep` blocks of
-// lowest rank are kept and written in ascending block order.  The whole
-// pooled-k column of block j is requested before the first product, so the
-// gate costs one memory round trip.
+// lowest rank are kept and written in ascending block order.
 template <int D, int MAXT>
 __global__ void __launch_bounds__(MAXT) k_gate_topk(IndexArgs a) {
   extern __shared__ uint64_t keys[];   // [T_b]
@@ -127,37 +162,14 @@ __global__ void __launch_bounds__(MAXT) k_gate_topk(IndexArgs a) {
   __syncthreads();
   uint64_t key = 0;
   if (j < tb) {
-    const double* qr = a.qb + (bh * tb + i) * D;   // the same row for every thread
-    const double* kc = a.kb + bh * D * tb + j;     // channel c of block j at kc[c * tb]
-    constexpr int BATCH = D < 64 ? D : 64;
-    double s = 0.0;
-#pragma unroll
-    for (int c0 = 0; c0 < D; c0 += BATCH) {
-      double kv[BATCH];
-#pragma unroll
-      for (int u = 0; u < BATCH; ++u) kv[u] = kc[(int64_t)(c0 + u) * tb];
-#pragma unroll
-      for (int u = 0; u < BATCH; ++u) {
-        const double p = __dmul_rn(qr[c0 + u], kv[u]);
-        s = (c0 + u == 0) ? p : __dadd_rn(s, p);
-      }
-    }
+    // the same query row for every thread; channel c of block j at kc[c * tb]
+    const double s = affinity_entry<D>(a.qb + (bh * tb + i) * D, a.kb + bh * D * tb + j, tb);
     if (!isfinite(s)) atomicOr(&bad, 1);
     key = rank_key(s);
     keys[j] = key;
   }
   __syncthreads();
-  bool kept = false;
-  if (MAXT == 64) {
-    kept = wave_topk(key, j < tb, a.keep, lane);   // one wave holds every key
-  } else if (j < tb) {
-    int rank = 0;
-    for (int jj = 0; jj < tb; ++jj) {
-      const uint64_t kj = keys[jj];
-      rank += (kj > key || (kj == key && jj < j)) ? 1 : 0;
-    }
-    kept = rank < a.keep;
-  }
+  const bool kept = rank_kept<MAXT>(key, j, tb, a.keep, keys);
   // Position of a kept block in the ascending list: kept blocks of lower id.
   const uint64_t mask = __ballot(kept);
   if (lane == 0) wave_kept[wave] = __popcll(mask);
@@ -172,6 +184,70 @@ __global__ void __launch_bounds__(MAXT) k_gate_topk(IndexArgs a) {
   if (j == 0) {
     out[0] = a.keep;
     a.flags[bh * tb + i] = bad;
+  }
+}
+
+// Head-shared gate, step 1: one workgroup per query block (i, h, b) writes
+// its row of the per-head affinity, S_h[i][j] for j < T_b, to srows.
+template <int D, int MAXT>
+__global__ void __launch_bounds__(MAXT) k_affinity_rows(IndexArgs a) {
+  int i, h, b;
+  unit_of(a, i, h, b);
+  const int tb = a.n_tiles, j = threadIdx.x;
+  const int64_t bh = (int64_t)b * a.heads + h;
+  if (j < tb)
+    a.srows[(bh * tb + i) * tb + j] = affinity_entry<D>(a.qb + (bh * tb + i) * D, a.kb + bh * D * tb + j, tb);
+}
+
+// Head-shared gate, step 2: one workgroup per query block (i, b); thread j
+// adds S_h[i][j] over heads h = 0, 1, ..., H-1 in that order (fp64), ranks
+// the sums and writes the same kept list and status flag for every head.
+template <int MAXT>
+__global__ void __launch_bounds__(MAXT) k_gate_shared(IndexArgs a) {
+  extern __shared__ uint64_t keys[];   // [T_b]
+  __shared__ int wave_kept[16];
+  __shared__ int bad;
+  const int tb = a.n_tiles;
+  const int b = blockIdx.x / tb, i = blockIdx.x - b * tb;
+  const int j = threadIdx.x, lane = j & 63, wave = j >> 6;
+  if (j == 0) bad = 0;
+  __syncthreads();
+  uint64_t key = 0;
+  if (j < tb) {
+    const double* col = a.srows + ((int64_t)b * a.heads * tb + i) * tb + j;   // head h at col[h * tb * tb]
+    const int64_t hstride = (int64_t)tb * tb;
+    double s = 0.0;
+    for (int h0 = 0; h0 < a.heads; h0 += 16) {
+      const int nh = min(16, a.heads - h0);
+      double v[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) v[u] = u < nh ? col[(h0 + u) * hstride] : 0.0;
+#pragma unroll
+      for (int u = 0; u < 16; ++u)
+        if (u < nh) s = (h0 + u == 0) ? v[u] : __dadd_rn(s, v[u]);
+    }
+    if (!isfinite(s)) atomicOr(&bad, 1);
+    key = rank_key(s);
+    keys[j] = key;
+  }
+  __syncthreads();
+  const bool kept = rank_kept<MAXT>(key, j, tb, a.keep, keys);
+  const uint64_t mask = __ballot(kept);
+  if (lane == 0) wave_kept[wave] = __popcll(mask);
+  __syncthreads();
+  int pos = __popcll(mask & ((1ull << lane) - 1ull));
+  for (int w = 0; w < wave; ++w) pos += wave_kept[w];
+  for (int h = 0; h < a.heads; ++h) {
+    const int64_t bh = (int64_t)b * a.heads + h;
+    int32_t* out = a.index + (bh * tb + i) * (tb + 1);
+    if (j < tb) {
+      if (kept) out[1 + pos] = j;
+      if (j >= a.keep) out[1 + j] = -1;
+    }
+    if (j == 0) {
+      out[0] = a.keep;
+      a.flags[bh * tb + i] = bad;
+    }
   }
 }
 
@@ -245,6 +321,25 @@ hipError_t launch_gate_topk(const IndexArgs& a, hipStream_t s) {
     if (block.x <= 64) hipLaunchKernelGGL((k_gate_topk<128, 64>), grid, block, lds, s, a);
     else if (block.x <= 256) hipLaunchKernelGGL((k_gate_topk<128, 256>), grid, block, lds, s, a);
     else hipLaunchKernelGGL((k_gate_topk<128, 1024>), grid, block, lds, s, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gate_topk_shared(const IndexArgs& a, hipStream_t s) {
+  dim3 grid_rows(a.n_tiles * a.heads * a.batch), grid_b(a.n_tiles * a.batch), block(round_threads(a.n_tiles));
+  const size_t lds = sizeof(uint64_t) * (size_t)a.n_tiles;
+  if (block.x <= 64) {
+    if (a.head_dim == 64) hipLaunchKernelGGL((k_affinity_rows<64, 64>), grid_rows, block, 0, s, a);
+    else hipLaunchKernelGGL((k_affinity_rows<128, 64>), grid_rows, block, 0, s, a);
+    hipLaunchKernelGGL((k_gate_shared<64>), grid_b, block, lds, s, a);
+  } else if (block.x <= 256) {
+    if (a.head_dim == 64) hipLaunchKernelGGL((k_affinity_rows<64, 256>), grid_rows, block, 0, s, a);
+    else hipLaunchKernelGGL((k_affinity_rows<128, 256>), grid_rows, block, 0, s, a);
+    hipLaunchKernelGGL((k_gate_shared<256>), grid_b, block, lds, s, a);
+  } else {
+    if (a.head_dim == 64) hipLaunchKernelGGL((k_affinity_rows<64, 1024>), grid_rows, block, 0, s, a);
+    else hipLaunchKernelGGL((k_affinity_rows<128, 1024>), grid_rows, block, 0, s, a);
+    hipLaunchKernelGGL((k_gate_shared<1024>), grid_b, block, lds, s, a);
   }
   return hipGetLastError();
 }

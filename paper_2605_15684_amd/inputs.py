@@ -23,7 +23,8 @@ from typing import Optional, Tuple
 
 import torch
 
-__all__ = ["Workload", "PRESETS", "preset", "make_qkv", "workload_from"]
+__all__ = ["Workload", "PRESETS", "preset", "make_qkv", "workload_from", "LAYER_KEEP_SCHEDULE_24",
+           "LAYER_SKIP_24"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -39,7 +40,7 @@ class Workload:
     tile: int
     n_text: int = 0
     dtype: str = "bf16"            # "bf16" or "f32": Q, K, V, O share it
-    gate: str = "topk"             # "topk", "window" or "dense"
+    gate: str = "topk"             # "topk", "topk_shared", "window" or "dense"
     keep: int = 0                  # topk: key tiles kept per query tile
     window: Tuple[int, int] = (1, 1)   # window gate: window size in tiles
     shift: Tuple[int, int] = (0, 0)    # roll of the token grid (y, x)
@@ -97,6 +98,19 @@ PRESETS = {
 # Sweep points over the 64-tile grid: masked fraction -> gate settings.
 SWEEP_TOPK_KEEP = {0.0: 64, 0.5: 32, 0.75: 16, 0.84375: 10, 0.9375: 4}
 SWEEP_WINDOW = {0.0: (8, 8), 0.5: (4, 8), 0.75: (4, 4), 0.9375: (2, 2)}
+
+
+# Per-layer kept blocks (of 64) for a 24-layer stack at 8x8 blocks on the
+# 64x64 grid.  The paper reports 84.16 % average sparsity for its
+# layer-importance-aware scheme (Table 2) without publishing the schedule;
+# this synthetic one keeps more blocks in the first and last layers and
+# averages 243 / (24 * 64) kept = 84.18 % masked.
+LAYER_KEEP_SCHEDULE_24 = (16, 13, 11, 10, 9, 9, 9, 9, 9, 9, 9, 9,
+                          8, 9, 9, 9, 9, 9, 9, 9, 10, 11, 13, 16)
+# Layers skipped by the depth-pruned stack used in the bench (every fourth
+# layer from layer 3; the paper's skipped blocks come from an unpublished
+# importance analysis).
+LAYER_SKIP_24 = tuple(l % 4 == 3 for l in range(24))
 
 
 def preset(name: str, **overrides) -> Workload:

@@ -21,10 +21,13 @@ from . import _lib
 _lib.load()   # fail loudly at import if the HIP library is missing
 
 __all__ = ["make_desc", "desc_for", "alloc_workspace", "build_index", "forward", "forward_dense",
-           "attention", "read_status", "layer_shift", "keep_from_rho", "SsbaError"]
+           "forward_topk", "forward_layers", "attention", "read_status", "layer_shift",
+           "keep_from_rho", "SsbaError"]
 
 SsbaError = _lib.SsbaError
-_GATES = {"topk": _lib.GATE_TOPK, "window": _lib.GATE_WINDOW, "dense": _lib.GATE_DENSE}
+_GATES = {"topk": _lib.GATE_TOPK, "window": _lib.GATE_WINDOW, "dense": _lib.GATE_DENSE,
+          "topk_shared": _lib.GATE_TOPK_SHARED}
+_TOPK = (_lib.GATE_TOPK, _lib.GATE_TOPK_SHARED)
 _DTYPES = {torch.bfloat16: _lib.DT_BF16, torch.float32: _lib.DT_F32}
 
 
@@ -102,8 +105,8 @@ def alloc_workspace(desc, device) -> Tuple[torch.Tensor, torch.Tensor]:
 
 
 def build_index(q, k, desc, index=None, scratch=None):
-    """Gate (top-k / window / dense) -> index.  Returns (index, scratch)."""
-    if desc.gate == _lib.GATE_TOPK:
+    """Gate (top-k / shared top-k / window / dense) -> index.  Returns (index, scratch)."""
+    if desc.gate in _TOPK:
         _check_tensors(desc, q, k)
         dev = q.device
     else:
@@ -114,8 +117,8 @@ def build_index(q, k, desc, index=None, scratch=None):
     if not (index.is_cuda and scratch.is_cuda and index.dtype == torch.int32 and index.is_contiguous()
             and index.numel() * 4 >= ib and scratch.numel() * scratch.element_size() >= sb):
         raise ValueError("index / scratch buffers too small or not on the GPU")
-    qp = q.data_ptr() if desc.gate == _lib.GATE_TOPK else None
-    kp = k.data_ptr() if desc.gate == _lib.GATE_TOPK else None
+    qp = q.data_ptr() if desc.gate in _TOPK else None
+    kp = k.data_ptr() if desc.gate in _TOPK else None
     _lib.check(_lib.build_index(desc, qp, kp, index.data_ptr(), scratch.data_ptr(), _stream(dev)),
                "ssba_build_index")
     return index, scratch
@@ -150,8 +153,8 @@ def forward_topk(q, k, v, desc, index=None, scratch=None, out=None):
     """Top-k gate and attention in one call (gate fused into the attention
     kernel where the shape allows).  Returns (index, scratch, out); index and
     scratch hold exactly what build_index would have left there."""
-    if desc.gate != _lib.GATE_TOPK:
-        raise ValueError("forward_topk needs the top-k gate")
+    if desc.gate not in _TOPK:
+        raise ValueError("forward_topk needs a top-k gate")
     if out is None:
         out = torch.empty_strided(q.shape, q.stride(), dtype=q.dtype, device=q.device)
     _check_tensors(desc, q, k, v, out)
@@ -164,6 +167,42 @@ def forward_topk(q, k, v, desc, index=None, scratch=None, out=None):
     _lib.check(_lib.forward_topk(desc, q.data_ptr(), k.data_ptr(), v.data_ptr(), index.data_ptr(),
                                  scratch.data_ptr(), out.data_ptr(), _stream(q.device)), "ssba_forward_topk")
     return index, scratch, out
+
+
+def forward_layers(layers, desc, index=None, scratch=None):
+    """A stack of SSBA layers in one call (ssba_forward_layers).
+
+    `layers`: sequence of dicts with q, k, v, out ([B, H, T, D] tensors laid
+    out as `desc` says), keep (top-k gates) and optional skip.  Layer l uses
+    desc's offset on even l and its negation on odd l.  Returns (index,
+    scratch): per-layer slices [L, B, H, T_b, 1 + T_b] and [L, stride]."""
+    n = len(layers)
+    ib, sb = _lib.layers_workspace_size(desc, n)
+    arr = (_lib.SsbaLayer * n)()
+    dev = None
+    for l, layer in enumerate(layers):
+        e = arr[l]
+        e.skip = 1 if layer.get("skip", False) else 0
+        e.keep = int(layer.get("keep", 0))
+        if e.skip:
+            continue
+        _check_tensors(desc, layer["q"], layer["k"], layer["v"], layer["out"])
+        dev = layer["q"].device
+        e.q, e.k, e.v, e.o = (layer[x].data_ptr() for x in ("q", "k", "v", "out"))
+    if dev is None:
+        dev = torch.device("cuda", torch.cuda.current_device())
+    tb = desc.grid_h * desc.grid_w // (desc.tile * desc.tile)
+    if index is None:
+        index = torch.empty((n, desc.batch, desc.heads, tb, tb + 1), dtype=torch.int32, device=dev)
+    if scratch is None:
+        scratch = torch.empty((n, sb // n // 8), dtype=torch.float64, device=dev)
+    if not (index.is_cuda and scratch.is_cuda and index.dtype == torch.int32 and index.is_contiguous()
+            and scratch.is_contiguous() and index.numel() * 4 >= ib
+            and scratch.numel() * scratch.element_size() >= sb):
+        raise ValueError("index / scratch buffers too small or not on the GPU")
+    _lib.check(_lib.forward_layers(desc, arr, index.data_ptr(), scratch.data_ptr(), _stream(dev)),
+               "ssba_forward_layers")
+    return index, scratch
 
 
 def read_status(desc, scratch) -> int:
@@ -182,11 +221,11 @@ def attention(q, k, v, *, grid, tile, shift=None, layer=None, rho=None, keep=Non
     if shift is None:
         shift = layer_shift(layer, tile) if layer is not None else (0, 0)
     tb = (grid[0] // tile) * (grid[1] // tile)
-    if gate == "topk" and keep is None:
+    if gate in ("topk", "topk_shared") and keep is None:
         keep = keep_from_rho(tb, 0.75 if rho is None else rho)
     desc = desc_for(q, grid=grid, tile=tile, shift=shift, n_text=n_text, gate=gate,
                     keep=keep or 0, window=window or (1, 1), scale=scale)
-    if gate == "topk":
+    if gate in ("topk", "topk_shared"):
         _, _, o = forward_topk(q, k, v, desc)
     else:
         index, _ = build_index(q, k, desc)

@@ -35,7 +35,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.ssba_abi_version() == 1
+    assert lib.ssba_abi_version() == 2
     seen = set()
     for s in range(7):
         txt = _lib.status_str(s)
@@ -64,6 +64,7 @@ def _desc(**kw):
      4 * 16 * 64 * 65, 16 * 16 * 64 * 128 + 4 * 16 * 64),
     ({"grid_h": 16, "grid_w": 16, "tile": 4, "heads": 2, "keep": 4, "dtype": _lib.DT_F32},
      4 * 2 * 16 * 17, 16 * 2 * 16 * 64 + 4 * 2 * 16),
+    ({"gate": _lib.GATE_TOPK_SHARED}, 4 * 16 * 64 * 65, 16 * 16 * 64 * 64 + 8 * 16 * 64 * 64 + 4 * 16 * 64),
 ])
 def test_workspace_sizes(lib, kw, index_bytes, scratch_bytes):
     assert _lib.workspace_size(_desc(**kw)) == (index_bytes, scratch_bytes)
@@ -151,3 +152,46 @@ def test_forward_kernel_name_of_invalid_descriptor(lib):
     assert _lib.forward_kernel(_desc(keep=0)) is None
     assert _lib.forward_kernel(_desc(keep=0), dense=True) == "k_attn_mfma<64, 3, true, false>"
     assert _lib.forward_kernel(_desc(head_dim=96)) is None
+
+
+@pytest.mark.parametrize("kw", [{}, {"gate": _lib.GATE_WINDOW, "win_h": 2, "win_w": 2},
+                                {"gate": _lib.GATE_TOPK_SHARED, "keep": 0}, {"keep": 0, "heads": 3}])
+def test_layers_workspace_size(lib, kw):
+    d = _desc(**kw)
+    one = _desc(**dict(kw, keep=1)) if "keep" in kw else d
+    ib1, sb1 = _lib.workspace_size(one)
+    for n in (1, 2, 24):
+        ib, sb = _lib.layers_workspace_size(d, n)
+        assert ib == n * ib1
+        assert sb == n * ((sb1 + 255) // 256 * 256)
+
+
+def test_layers_bad_arguments_rejected_before_launch(lib):
+    d = _desc()
+    fake = 1 << 20                                   # aligned, never dereferenced: rejected first
+    layers = (_lib.SsbaLayer * 3)()
+    for e in layers:
+        e.q = e.k = e.v = e.o = fake
+        e.keep = 10
+    assert lib.ssba_forward_layers(ctypes.byref(d), layers, 0, fake, fake, None) == _lib.SSBA_ERR_ARG
+    assert lib.ssba_forward_layers(ctypes.byref(d), None, 3, fake, fake, None) == _lib.SSBA_ERR_ARG
+    assert lib.ssba_forward_layers(None, layers, 3, fake, fake, None) == _lib.SSBA_ERR_ARG
+    assert lib.ssba_forward_layers(ctypes.byref(d), layers, 3, None, fake, None) == _lib.SSBA_ERR_ARG
+    assert lib.ssba_forward_layers(ctypes.byref(d), layers, 3, fake, None, None) == _lib.SSBA_ERR_ARG
+    layers[2].keep = 65                              # keep beyond T_b in the last layer
+    assert lib.ssba_forward_layers(ctypes.byref(d), layers, 3, fake, fake, None) == _lib.SSBA_ERR_ARG
+    layers[2].skip = 1                               # ... unless that layer is skipped: then a null
+    layers[1].q = None                               # q in layer 1 is still caught
+    assert lib.ssba_forward_layers(ctypes.byref(d), layers, 3, fake, fake, None) == _lib.SSBA_ERR_ARG
+    layers[1].q = fake + 8                           # misaligned bf16 rows
+    assert lib.ssba_forward_layers(ctypes.byref(d), layers, 3, fake, fake, None) == _lib.SSBA_ERR_ARG
+    bad = _desc(grid_h=60)
+    layers[1].q = fake
+    assert lib.ssba_forward_layers(ctypes.byref(bad), layers, 3, fake, fake, None) == _lib.SSBA_ERR_SHAPE
+
+
+def test_shared_gate_names_two_call_kernel(lib):
+    """The shared gate runs the two calls inside ssba_forward_topk: mode 2
+    names the ungated attention kernel."""
+    assert _lib.forward_kernel(_desc(gate=_lib.GATE_TOPK_SHARED), mode=2) == "k_attn_mfma<64, 3, false, false>"
+    assert _lib.forward_kernel(_desc(), mode=2) == "k_attn_mfma<64, 3, false, true>"

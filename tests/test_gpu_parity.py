@@ -309,3 +309,135 @@ def test_forward_topk_nonfinite_sets_status():
     kg2[0, 1, 100, 5] = float("nan")
     _, scratch, _ = ssba.forward_topk(qg, kg2, vg, desc)
     assert ssba.read_status(desc, scratch) == 5
+
+
+# ------------------------------------------------ head-shared top-k gate --
+SHARED_CASES = [
+    preset("grid64", heads=4, gate="topk_shared"),
+    preset("grid64_text", batch=2, heads=3, gate="topk_shared"),
+    preset("grid128", heads=3, gate="topk_shared"),                       # D 128, 16x16 blocks
+    workload_from(batch=1, heads=5, grid_h=128, grid_w=128, head_dim=64, tile=8, keep=30,
+                  shift=(-4, 4), gate="topk_shared"),                      # T_b 256
+    workload_from(batch=2, heads=2, grid_h=48, grid_w=40, head_dim=64, tile=8, keep=7, shift=(3, 5),
+                  n_text=13, gate="topk_shared"),                          # T_b 30
+    preset("tiny", gate="topk_shared"),                                    # fp32
+]
+
+
+@pytest.mark.parametrize("w", SHARED_CASES, ids=_ids)
+def test_shared_gate_index_bit_exact(w):
+    (q, k, _), (qg, kg, _) = inputs(w)
+    from paper_2605_15684_amd import ssba
+    desc = gpu_desc(w, qg)
+    index, scratch = ssba.build_index(qg, kg, desc)
+    got = index.cpu().numpy()
+    want = oracle_index(w, q, k)
+    assert np.array_equal(got, want)
+    assert (got == got[:, :1]).all()              # every head holds the same lists
+    assert ssba.read_status(desc, scratch) == 0
+
+
+@pytest.mark.parametrize("w", SHARED_CASES[:2] + SHARED_CASES[-1:], ids=_ids)
+def test_shared_gate_forward_topk_and_output(w):
+    """forward_topk with the shared gate equals build_index + forward, and the
+    output matches the oracle on every row (small) or sampled rows."""
+    from paper_2605_15684_amd import ssba
+    (q, k, v), (qg, kg, vg) = inputs(w)
+    desc = gpu_desc(w, qg)
+    index2, _ = ssba.build_index(qg, kg, desc)
+    out2 = ssba.forward(qg, kg, vg, index2, desc)
+    index1, _, out1 = ssba.forward_topk(qg, kg, vg, desc)
+    torch.cuda.synchronize()
+    assert torch.equal(index1, index2) and torch.equal(out1, out2)
+    want_idx = oracle_index(w, q, k)
+    rng = np.random.default_rng(3)
+    heads = [(b, h) for b in range(w.batch) for h in range(w.heads)][:4]
+    rows = sample_rows(w, rng)
+    ref = O.attention(to64(q), to64(k), to64(v), want_idx, rows=rows, heads=heads, **oracle_kw(w))
+    assert max_err(out1, ref, heads, rows) <= tol(w)
+
+
+def test_shared_gate_nonfinite_sets_status():
+    from paper_2605_15684_amd import ssba
+    w = preset("grid64", heads=3, gate="topk_shared")
+    (_, _, _), (qg, kg, _) = inputs(w)
+    desc = gpu_desc(w, qg)
+    kg2 = kg.clone()
+    kg2[0, 2, 700, 1] = float("inf")
+    _, scratch = ssba.build_index(qg, kg2, desc)
+    assert ssba.read_status(desc, scratch) == 5
+
+
+# ------------------------------------------------------------ layer stack --
+def _layer_stack(w, keeps, skips, seed0=11):
+    """Per-layer seeded inputs (seed seed0 + l) of workload w."""
+    layers = []
+    for l, (kp, sk) in enumerate(zip(keeps, skips)):
+        (q, k, v), (qg, kg, vg) = inputs(w.with_(seed=seed0 + l))
+        out = torch.full_like(qg, 7.0)
+        layers.append(dict(q=qg, k=kg, v=vg, out=out, keep=kp, skip=sk, cpu=(q, k, v)))
+    return layers
+
+
+@pytest.mark.parametrize("gate,window", [("topk", (1, 1)), ("topk_shared", (1, 1)), ("window", (2, 2)),
+                                         ("dense", (1, 1))])
+def test_layer_stack_equals_per_layer_calls(gate, window):
+    """ssba_forward_layers == one call per layer with the layer's offset
+    (negated on odd layers) and keep; skipped layers leave their output
+    untouched; static gates reuse one index per offset parity."""
+    from paper_2605_15684_amd import ssba
+    w = preset("grid64", heads=2, n_text=0, gate=gate, window=window, shift=(4, 4))
+    keeps = [10, 16, 4, 10, 7]
+    skips = [False, False, True, False, False]
+    layers = _layer_stack(w, keeps, skips)
+    desc = gpu_desc(w, layers[0]["q"])
+    index, scratch = ssba.forward_layers(layers, desc)
+    torch.cuda.synchronize()
+    for l, L in enumerate(layers):
+        if L["skip"]:
+            assert bool((L["out"] == 7.0).all())
+            continue
+        sh = (4, 4) if l % 2 == 0 else (-4, -4)
+        wl = w.with_(shift=sh, keep=keeps[l])
+        dl = gpu_desc(wl, L["q"])
+        if gate in ("topk", "topk_shared"):
+            idx1, _, out1 = ssba.forward_topk(L["q"], L["k"], L["v"], dl)
+            assert torch.equal(index[l], idx1)
+        else:
+            idx1, _ = ssba.build_index(None, None, dl)
+            out1 = ssba.forward(L["q"], L["k"], L["v"], idx1, dl)
+        torch.cuda.synchronize()
+        assert torch.equal(L["out"], out1), f"layer {l}"
+        if gate in ("topk", "topk_shared"):
+            dl_status = gpu_desc(wl, L["q"])
+            assert ssba.read_status(dl_status, scratch[l]) == 0
+
+
+def test_layer_stack_against_oracle_and_status():
+    """Three layers at the 64x64 size against the oracle's layer stack
+    (sampled rows), with a NaN in layer 1 reported by that layer's scratch
+    slice only."""
+    from paper_2605_15684_amd import ssba
+    w = preset("grid64", heads=2)
+    keeps, skips = [10, 12, 8], [False, False, False]
+    layers = _layer_stack(w, keeps, skips, seed0=21)
+    layers[1]["k"][0, 1, 333, 7] = float("nan")
+    desc = gpu_desc(w, layers[0]["q"])
+    index, scratch = ssba.forward_layers(layers, desc)
+    torch.cuda.synchronize()
+    statuses = [ssba.read_status(desc, scratch[l]) for l in range(3)]
+    assert statuses == [0, 5, 0]
+    ol = [dict(q=to64(L["cpu"][0]), k=to64(L["cpu"][1]), v=to64(L["cpu"][2]), keep=L["keep"])
+          for L in layers]
+    for l in (0, 2):   # the NaN layer is only checked through its status
+        sh = O.layer_shift(l, w.tile)
+        want_idx = O.build_index(ol[l]["q"], ol[l]["k"], gate="topk", keep=keeps[l], grid_h=w.grid_h,
+                                 grid_w=w.grid_w, tile=w.tile, shift=sh, n_text=0)
+        assert np.array_equal(index[l].cpu().numpy(), want_idx)
+        rng = np.random.default_rng(l)
+        wl = w.with_(shift=sh)
+        rows = sample_rows(wl, rng, n_random=32)
+        heads = [(0, 0), (0, 1)]
+        ref = O.attention(ol[l]["q"], ol[l]["k"], ol[l]["v"], want_idx, rows=rows, heads=heads,
+                          **oracle_kw(wl))
+        assert max_err(layers[l]["out"], ref, heads, rows) <= BF16_TOL
