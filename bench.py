@@ -1,7 +1,7 @@
 """Benchmark of the SSBA forward path on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload grid64]
-                    [--no-cpu] [--sweep] [--copy-calibration] [--layers]
+                    [--no-cpu] [--sweep] [--copy-calibration] [--layers] [--haar]
 
 One step = one SSBA layer call on inputs already resident in HBM: the top-k
 gate (block pooling, affinity, ranking -> index) and the block-sparse
@@ -38,6 +38,10 @@ masked, the offset alternating with layer parity, distinct inputs per layer):
 the stack, the same layers as separate calls, a depth-pruned stack, the
 head-shared gate and the window gate with its per-parity index cache.
 
+--haar prints instead one JSON line for the multi-level Haar transform pair
+(T-DVAE wavelets) on a [1, 128, 512, 512] bf16 feature map, 3 levels: the
+forward and inverse launch times and their GB/s against the HBM roofline.
+
 --copy-calibration runs only that plain copy (256 MiB, 5 times) for the
 counter runs and prints its size.
 """
@@ -66,6 +70,9 @@ COPY_BYTES = 256 << 20
 # factors (bytes known / bytes the counter reads for a plain 256 MiB copy).
 # From the counter summary in profiles/k_attn_mfma_grid64.md.
 MEASURED_TRAFFIC = {
+    ("k_haar_dwt<unsigned short, 3>", "haar512"): {"sha": "02be9c317bd1aa8b", "fetch_kib": 131115.0,
+                                                  "write_kib": 344064.0, "fetch_factor": 1.9998,
+                                                  "write_factor": 1.0},
     ("k_attn_mfma<64, 3, false, false>", "grid64"): {"sha": "5fbf4ac2f235c356", "fetch_kib": 12501.5,
                                                      "write_kib": 8192.0, "fetch_factor": 1.9998,
                                                      "write_factor": 1.0},
@@ -73,8 +80,11 @@ MEASURED_TRAFFIC = {
 
 def kernel_sources(kernel: str):
     base = os.path.join(ROOT, "paper_2605_15684_amd", "csrc")
+    stem = kernel.split("<")[0]
+    if stem in ("k_haar_dwt", "k_haar_iwt"):
+        return [os.path.join(base, "ssba_haar.hip"), os.path.join(ROOT, "include", "ssba_haar.h")]
     own = {"k_attn_mfma": "ssba_attn_mfma.hip", "k_attn_bf16": "ssba_attn_bf16.hip",
-           "k_attn_f32": "ssba_attn_f32.hip"}[kernel.split("<")[0]]
+           "k_attn_f32": "ssba_attn_f32.hip"}[stem]
     return [os.path.join(base, own), os.path.join(base, "ssba_common.h"),
             os.path.join(ROOT, "include", "ssba.h")]
 
@@ -369,6 +379,109 @@ def measure_layers(w, steps: int, warmup: int) -> dict:
     }
 
 
+HAAR_SHAPE, HAAR_LEVELS = (4, 128, 512, 512), 3
+PEAK_HBM_GBS = 8000.0
+
+
+def haar_bytes(shape, levels: int, elem: int = 2):
+    """Algorithmic HBM bytes: forward reads x and writes every level's four
+    bands; inverse reads the coarsest LL and every level's three detail bands
+    and writes the output."""
+    n, c, h, w = shape
+    x = n * c * h * w * elem
+    lv = [n * 4 * c * (h >> l) * (w >> l) * elem for l in range(1, levels + 1)]
+    fwd = x + sum(lv)
+    inv = lv[-1] // 4 + sum(3 * b // 4 for b in lv) + x
+    return fwd, inv
+
+
+def measure_haar(steps: int, warmup: int, with_cpu: bool) -> dict:
+    """The multi-level Haar transform pair of the Tiny DWT-Distilled VAE on
+    four [128, 512, 512] bf16 feature maps, 3 levels (synthetic: the paper
+    gives no channel count).  The 592 MiB a forward call touches exceed the
+    256 MB MALL, so back-to-back calls stream from HBM."""
+    import torch
+    from paper_2605_15684_amd import _lib, haar
+    g = torch.Generator(device="cpu").manual_seed(1)
+    x = torch.randn(HAAR_SHAPE, generator=g, dtype=torch.float32).to(torch.bfloat16).to("cuda")
+    lv = haar.dwt(x, HAAR_LEVELS)
+    y = torch.empty_like(x)
+
+    def span(fn, n):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    ms_dwt = span(lambda: haar.dwt(x, HAAR_LEVELS, out=lv), steps)
+    ms_iwt = span(lambda: haar.iwt(lv, out=y), steps)
+
+    # Cold single calls: a 1 GiB write before each evicts whatever part of
+    # the working set the MALL still holds.
+    evict = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+
+    def cold(fn, reps=10):
+        ts = []
+        for r in range(reps):
+            evict.fill_(float(r))
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return sorted(ts)[reps // 2]
+    ms_dwt_cold = cold(lambda: haar.dwt(x, HAAR_LEVELS, out=lv))
+    ms_iwt_cold = cold(lambda: haar.iwt(lv, out=y))
+    del evict
+    # Reference: a plain device copy of x (read + write of 256 MiB), the
+    # streaming rate a kernel can reach on this box.
+    ms_copy = span(lambda: y.copy_(x), steps)
+    gbs_copy = 2 * x.numel() * x.element_size() / (ms_copy * 1e-3) / 1e9
+    b_fwd, b_inv = haar_bytes(HAAR_SHAPE, HAAR_LEVELS)
+    gbs_dwt = b_fwd / (ms_dwt * 1e-3) / 1e9
+    gbs_iwt = b_inv / (ms_iwt * 1e-3) / 1e9
+    desc = haar.haar_desc(HAAR_SHAPE, HAAR_LEVELS, torch.bfloat16)
+    kernel = _lib.haar_kernel_name(desc, False)
+    traffic = measured_traffic(kernel, "haar512")
+    line = {
+        "metric": "Haar DWT GB/s (T-DVAE multi-level Haar transform, HBM roofline)",
+        "value": round(gbs_dwt, 1), "unit": "GB/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
+        "ms_per_step": round(ms_dwt, 5), "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"haar512: x [4, 128, 512, 512] bf16, {HAAR_LEVELS} levels, all four bands "
+                               "stored per level"},
+        "ms_dwt": round(ms_dwt, 5), "ms_iwt": round(ms_iwt, 5),
+        "gbs_iwt": round(gbs_iwt, 1), "bytes_dwt": b_fwd, "bytes_iwt": b_inv,
+        "gbs_device_copy": round(gbs_copy, 1),
+        "ms_dwt_cold": round(ms_dwt_cold, 5), "ms_iwt_cold": round(ms_iwt_cold, 5),
+        "gbs_dwt_cold": round(b_fwd / (ms_dwt_cold * 1e-3) / 1e9, 1),
+        "gbs_iwt_cold": round(b_inv / (ms_iwt_cold * 1e-3) / 1e9, 1),
+        "roofline": {"bound": "hbm", "kernel": kernel, "achieved": round(gbs_dwt, 1), "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(gbs_dwt / PEAK_HBM_GBS, 4),
+                     "traffic": None if traffic is None else round(traffic),
+                     "traffic_unit": "HBM bytes/launch", "sources_sha": sources_sha(kernel)},
+        "roofline_iwt": {"bound": "hbm", "kernel": _lib.haar_kernel_name(desc, True),
+                         "achieved": round(gbs_iwt, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": round(gbs_iwt / PEAK_HBM_GBS, 4)},
+    }
+    if with_cpu:
+        from oracle import haar_oracle as H
+        xc = x[:1, :8].float().cpu().double().numpy()
+        t0 = time.perf_counter()
+        H.dwt(xc, HAAR_LEVELS)
+        sec = time.perf_counter() - t0
+        line["cpu_baseline"] = {"value": round(b_fwd / 64 / sec / 1e9, 3), "unit": "GB/s", "cores": 1,
+                                "kind": "oracle",
+                                "sample": f"fp64 oracle forward on 8 of 512 planes ({sec:.2f} s), pro-rated"}
+    return line
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -380,6 +493,8 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--layers", action="store_true",
                     help="measure the 24-layer stack (ssba_forward_layers) instead of one call")
+    ap.add_argument("--haar", action="store_true",
+                    help="measure the multi-level Haar transform pair instead of the SSBA call")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the SSBA path has no multi-GPU mode in this build "
@@ -398,6 +513,9 @@ def main():
         print(json.dumps({"copy_bytes": COPY_BYTES, "calls": 5}), flush=True)
         return
 
+    if args.haar:
+        print(json.dumps(measure_haar(args.steps, args.warmup, not args.no_cpu)), flush=True)
+        return
     w = preset(args.workload)
     if args.layers:
         print(json.dumps(measure_layers(w, max(5, args.steps // 10), max(2, args.warmup // 10))), flush=True)

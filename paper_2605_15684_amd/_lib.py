@@ -29,7 +29,7 @@ GATE_TOPK_SHARED = 3
 EXPORTS = ("ssba_abi_version", "ssba_status_str", "ssba_workspace_size", "ssba_build_index",
            "ssba_forward", "ssba_forward_dense", "ssba_read_device_status",
            "ssba_forward_kernel", "ssba_forward_topk", "ssba_layers_workspace_size",
-           "ssba_forward_layers")
+           "ssba_forward_layers", "ssba_haar_dwt", "ssba_haar_iwt", "ssba_haar_kernel_name")
 
 
 class SsbaDesc(ctypes.Structure):
@@ -47,6 +47,11 @@ class SsbaDesc(ctypes.Structure):
 class SsbaLayer(ctypes.Structure):
     _fields_ = [("q", ctypes.c_void_p), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
                 ("o", ctypes.c_void_p), ("keep", ctypes.c_int32), ("skip", ctypes.c_int32)]
+
+
+class HaarDesc(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("c", ctypes.c_int32), ("h", ctypes.c_int32), ("w", ctypes.c_int32),
+                ("levels", ctypes.c_int32), ("dtype", ctypes.c_int32)]
 
 
 class SsbaError(RuntimeError):
@@ -98,6 +103,13 @@ def load(path: str = None) -> ctypes.CDLL:
     lib.ssba_layers_workspace_size.argtypes = [dp, ctypes.c_int, ctypes.POINTER(sz), ctypes.POINTER(sz)]
     lib.ssba_forward_layers.restype = ctypes.c_int
     lib.ssba_forward_layers.argtypes = [dp, ctypes.POINTER(SsbaLayer), ctypes.c_int, vp, vp, vp]
+    hp = ctypes.POINTER(HaarDesc)
+    lib.ssba_haar_dwt.restype = ctypes.c_int
+    lib.ssba_haar_dwt.argtypes = [hp, vp, ctypes.POINTER(vp), vp]
+    lib.ssba_haar_iwt.restype = ctypes.c_int
+    lib.ssba_haar_iwt.argtypes = [hp, ctypes.POINTER(vp), ctypes.POINTER(vp), vp, vp]
+    lib.ssba_haar_kernel_name.restype = ctypes.c_char_p
+    lib.ssba_haar_kernel_name.argtypes = [hp, ctypes.c_int]
     lib.ssba_read_device_status.restype = ctypes.c_int
     lib.ssba_read_device_status.argtypes = [dp, vp, ctypes.POINTER(ctypes.c_int), vp]
     _lib = lib
@@ -163,3 +175,19 @@ def forward_layers(desc, layers, index_ptr, scratch_ptr, stream) -> int:
     """`layers`: a ctypes array of SsbaLayer."""
     return load().ssba_forward_layers(ctypes.byref(desc), layers, len(layers), index_ptr, scratch_ptr,
                                       stream)
+
+
+def haar_dwt(desc, x_ptr, level_ptrs, stream) -> int:
+    arr = (ctypes.c_void_p * max(1, len(level_ptrs)))(*level_ptrs)
+    return load().ssba_haar_dwt(ctypes.byref(desc), x_ptr, arr, stream)
+
+
+def haar_iwt(desc, level_ptrs, residual_ptrs, x_ptr, stream) -> int:
+    arr = (ctypes.c_void_p * max(1, len(level_ptrs)))(*level_ptrs)
+    res = None if residual_ptrs is None else (ctypes.c_void_p * max(1, len(residual_ptrs)))(*residual_ptrs)
+    return load().ssba_haar_iwt(ctypes.byref(desc), arr, res, x_ptr, stream)
+
+
+def haar_kernel_name(desc, inverse: bool):
+    name = load().ssba_haar_kernel_name(ctypes.byref(desc), 1 if inverse else 0)
+    return None if name is None else name.decode()

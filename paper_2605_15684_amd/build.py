@@ -27,6 +27,7 @@ SOURCES = {
     # MFMA results in ordinary VGPRs: the softmax reads every score and the
     # default accumulation-register form costs a copy per element.
     "ssba_attn_mfma.hip": ["-ffp-contract=off", "-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "ssba_haar.hip": ["-ffp-contract=off"],
 }
 
 COMMON = [

@@ -2,6 +2,7 @@
 library loads, exports every function include/ssba.h declares, sizes its
 workspace as documented and rejects bad descriptors before any launch."""
 import ctypes
+import glob
 import os
 import re
 
@@ -10,7 +11,7 @@ import pytest
 from paper_2605_15684_amd import _lib
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "ssba.h")
+HEADERS = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 
 
 @pytest.fixture(scope="module")
@@ -22,7 +23,7 @@ def lib():
 
 
 def _declared_functions():
-    text = open(HEADER).read()
+    text = "\n".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(ssba_[a-z_]+)\s*\(", text)))
 
@@ -195,3 +196,45 @@ def test_shared_gate_names_two_call_kernel(lib):
     names the ungated attention kernel."""
     assert _lib.forward_kernel(_desc(gate=_lib.GATE_TOPK_SHARED), mode=2) == "k_attn_mfma<64, 3, false, false>"
     assert _lib.forward_kernel(_desc(), mode=2) == "k_attn_mfma<64, 3, false, true>"
+
+
+def _hdesc(**kw):
+    d = _lib.HaarDesc()
+    base = dict(n=1, c=128, h=512, w=512, levels=3, dtype=_lib.DT_BF16)
+    base.update(kw)
+    for k, v in base.items():
+        setattr(d, k, v)
+    return d
+
+
+@pytest.mark.parametrize("kw,status", [
+    ({"n": 0}, _lib.SSBA_ERR_SHAPE), ({"c": -1}, _lib.SSBA_ERR_SHAPE),
+    ({"h": 12}, _lib.SSBA_ERR_SHAPE),                   # not a multiple of 2^3
+    ({"w": 20}, _lib.SSBA_ERR_SHAPE),                   # not a multiple of 8
+    ({"levels": 0}, _lib.SSBA_ERR_UNSUPPORTED), ({"levels": 4}, _lib.SSBA_ERR_UNSUPPORTED),
+    ({"dtype": 5}, _lib.SSBA_ERR_ARG),
+])
+def test_haar_bad_descriptors_rejected_before_launch(lib, kw, status):
+    d = _hdesc(**kw)
+    fake = 1 << 20
+    assert _lib.haar_dwt(d, fake, [fake] * 3, None) == status
+    assert _lib.haar_iwt(d, [fake] * 3, None, fake, None) == status
+    assert _lib.haar_kernel_name(d, False) is None
+
+
+def test_haar_null_and_misaligned_pointers_rejected(lib):
+    d = _hdesc()
+    fake = 1 << 20
+    assert _lib.haar_dwt(d, None, [fake] * 3, None) == _lib.SSBA_ERR_ARG
+    assert _lib.haar_dwt(d, fake, [fake, None, fake], None) == _lib.SSBA_ERR_ARG
+    assert _lib.haar_dwt(d, fake + 2, [fake] * 3, None) == _lib.SSBA_ERR_ARG
+    assert lib.ssba_haar_dwt(ctypes.byref(d), fake, None, None) == _lib.SSBA_ERR_ARG
+    assert _lib.haar_iwt(d, [fake] * 3, None, None, None) == _lib.SSBA_ERR_ARG
+    assert _lib.haar_iwt(d, [fake, fake, fake + 8], None, fake, None) == _lib.SSBA_ERR_ARG
+    assert _lib.haar_iwt(d, [fake] * 3, [None, fake + 4, None], fake, None) == _lib.SSBA_ERR_ARG
+    assert lib.ssba_haar_dwt(None, fake, None, None) == _lib.SSBA_ERR_ARG
+
+
+def test_haar_kernel_names(lib):
+    assert _lib.haar_kernel_name(_hdesc(), False) == "k_haar_dwt<unsigned short, 3>"
+    assert _lib.haar_kernel_name(_hdesc(levels=1, dtype=_lib.DT_F32), True) == "k_haar_iwt<float, 1>"
