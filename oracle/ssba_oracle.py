@@ -30,6 +30,9 @@ Steps, in the paper's order and notation:
                ones (Section 2.2.1; Algorithm 1, expand and pad steps).
   attention -- masked softmax attention over [text; image] in fp64
                (Algorithm 1, attention step).
+  backward  -- gradients of the attention with respect to Q, K and V with the
+               gate held fixed (the kept lists carry no gradient), the
+               per-row log-sum-exp, and the key-block view of an index.
 
 Readings where the paper is silent (each also listed in the design notes):
 k counts dropped blocks per query row; sums rather than means are ranked; ties
@@ -305,3 +308,62 @@ def ssba_layers(layers, *, grid_h, grid_w, tile, shift=None, n_text=0, gate="top
                         tile=tile, shift=sh, n_text=n_text, gate=gate,
                         keep=layer.get("keep", 0), window=window, scale=scale))
     return out
+
+
+# --------------------------------------------------------------------------
+# Backward pass of the attend step (gradients of Algorithm 1's attention
+# with the gate held fixed: the kept lists carry no gradient).
+# --------------------------------------------------------------------------
+def transpose_index(index: np.ndarray) -> np.ndarray:
+    """Key-block view of an index: entry [b, h, j] lists, ascending, the query
+    blocks i whose kept list holds j (same canonical layout: count, ids, -1)."""
+    b_n, h_n, tb = index.shape[:3]
+    lists = []
+    for b in range(b_n):
+        per_h = []
+        for h in range(h_n):
+            seen = [[] for _ in range(tb)]
+            for i in range(tb):
+                for j in index[b, h, i, 1:1 + int(index[b, h, i, 0])]:
+                    seen[int(j)].append(i)
+            per_h.append([np.array(s, dtype=np.int64) for s in seen])
+        lists.append(per_h)
+    return pack_index(lists, tb)
+
+
+def attention_backward(q, k, v, dout, index, *, grid_h, grid_w, tile, shift=(0, 0), n_text=0,
+                       scale=None, heads=None):
+    """Gradients of the SSBA attention output with respect to Q, K and V, fp64.
+
+    With P = softmax(scale Q K^T + mask) over the token mask of the index
+    (text rows and columns visible), and the upstream gradient dO:
+      dV = P^T dO,  dP = dO V^T,  dS = P * (dP - rowsum(P * dP)),
+      dQ = scale dS K,  dK = scale dS^T Q;
+    also the natural-log log-sum-exp of each row's masked scaled logits.
+    Returns (dq, dk, dv, lse); pairs outside ``heads`` are left NaN.
+    """
+    b_n, h_n, t, c = q.shape
+    if scale is None or scale <= 0:
+        scale = 1.0 / math.sqrt(c)
+    dq = np.full(q.shape, np.nan)
+    dk = np.full(q.shape, np.nan)
+    dv = np.full(q.shape, np.nan)
+    lse = np.full((b_n, h_n, t), np.nan)
+    pairs = [(b, h) for b in range(b_n) for h in range(h_n)] if heads is None else list(heads)
+    rows = np.arange(t)
+    for b, h in pairs:
+        qq, kk, vv, gg = (np.asarray(x[b, h], np.float64) for x in (q, k, v, dout))
+        mask = token_mask_rows(index[b, h], rows, grid_h=grid_h, grid_w=grid_w, tile=tile,
+                               shift=shift, n_text=n_text)
+        logits = np.where(mask, scale * (qq @ kk.T), -np.inf)
+        m = logits.max(axis=-1, keepdims=True)
+        e = np.exp(logits - m)
+        s = e.sum(axis=-1, keepdims=True)
+        p = e / s
+        lse[b, h] = (m + np.log(s))[:, 0]
+        dp = gg @ vv.T
+        ds = p * (dp - np.sum(p * dp, axis=-1, keepdims=True))
+        dv[b, h] = p.T @ gg
+        dq[b, h] = scale * (ds @ kk)
+        dk[b, h] = scale * (ds.T @ qq)
+    return dq, dk, dv, lse
