@@ -2,6 +2,7 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload grid64]
                     [--no-cpu] [--sweep] [--copy-calibration] [--layers] [--haar]
+                    [--backward]
 
 One step = one SSBA layer call on inputs already resident in HBM: the top-k
 gate (block pooling, affinity, ranking -> index) and the block-sparse
@@ -41,6 +42,10 @@ head-shared gate and the window gate with its per-parity index cache.
 --haar prints instead one JSON line for the multi-level Haar transform pair
 (T-DVAE wavelets) on a [1, 128, 512, 512] bf16 feature map, 3 levels: the
 forward and inverse launch times and their GB/s against the HBM roofline.
+
+--backward prints instead one JSON line for a training step of the call:
+the forward with its log-sum-exp and the backward (dQ, dK, dV with the gate
+held fixed), TFLOP/s counting 10 D flops per computed pair in the backward.
 
 --copy-calibration runs only that plain copy (256 MiB, 5 times) for the
 counter runs and prints its size.
@@ -482,6 +487,58 @@ def measure_haar(steps: int, warmup: int, with_cpu: bool) -> dict:
     return line
 
 
+def measure_backward(w, steps: int, warmup: int) -> dict:
+    """Training step of one SSBA layer on the 64x64 grid: the forward with
+    its log-sum-exp, then the backward (gradients of the attend step with the
+    gate held fixed).  Algorithmic work: 4 D flops per computed pair in the
+    forward, 10 D in the backward (dV = P^T dO, dP = dO V^T, dQ = dS K,
+    dK = dS^T Q and the recomputed scores)."""
+    import torch
+    from paper_2605_15684_amd import _lib, ssba
+    from paper_2605_15684_amd.inputs import make_qkv
+    q, k, v = make_qkv(w, device="cuda")
+    desc = ssba.desc_for(q, grid=(w.grid_h, w.grid_w), tile=w.tile, shift=w.shift, n_text=w.n_text,
+                         gate=w.gate, keep=w.keep)
+    index, _ = ssba.build_index(q, k, desc)
+    out, lse = ssba.forward_train(q, k, v, index, desc)
+    g = torch.Generator(device="cpu").manual_seed(w.seed + 7)
+    dout = torch.randn(q.shape, generator=g, dtype=torch.float32).to(torch.bfloat16).to("cuda")
+    dq, dk, dv = (torch.empty_like(q) for _ in range(3))
+    sb = _lib.backward_workspace_size(desc)
+    scratch = torch.empty(((sb + 7) // 8,), dtype=torch.float64, device="cuda")
+
+    def span(fn, n):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    ms_fwd = span(lambda: ssba.forward_train(q, k, v, index, desc, out, lse), steps)
+    ms_bwd = span(lambda: ssba.backward(q, k, v, out, dout, lse, index, desc, dq, dk, dv, scratch), steps)
+    f_fwd = flops(w)
+    f_bwd = 2.5 * f_fwd
+    tf_bwd = f_bwd / (ms_bwd * 1e-3) / 1e12
+    return {
+        "metric": "SSBA backward TFLOP/s (gradients of the attend step, 4096 tokens, 84% sparse)",
+        "value": round(tf_bwd, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
+        "ms_per_step": round(ms_bwd, 5), "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{w.name}: {describe(w)}"},
+        "ms_forward_train": round(ms_fwd, 5), "ms_backward": round(ms_bwd, 5),
+        "ms_train_step": round(ms_fwd + ms_bwd, 5),
+        "tflops_train_step": round((f_fwd + f_bwd) / ((ms_fwd + ms_bwd) * 1e-3) / 1e12, 2),
+        "gflop_backward": round(f_bwd / 1e9, 3),
+        "roofline": {"bound": "mfma", "kernel": "k_bwd_dq + k_bwd_dkdv (+ pre-pass, transpose)",
+                     "achieved": round(tf_bwd, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tf_bwd / PEAK_BF16_TFLOPS, 4)},
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -495,6 +552,8 @@ def main():
                     help="measure the 24-layer stack (ssba_forward_layers) instead of one call")
     ap.add_argument("--haar", action="store_true",
                     help="measure the multi-level Haar transform pair instead of the SSBA call")
+    ap.add_argument("--backward", action="store_true",
+                    help="measure the training forward and the backward of one SSBA call")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the SSBA path has no multi-GPU mode in this build "
@@ -517,6 +576,9 @@ def main():
         print(json.dumps(measure_haar(args.steps, args.warmup, not args.no_cpu)), flush=True)
         return
     w = preset(args.workload)
+    if args.backward:
+        print(json.dumps(measure_backward(w, args.steps, args.warmup)), flush=True)
+        return
     if args.layers:
         print(json.dumps(measure_layers(w, max(5, args.steps // 10), max(2, args.warmup // 10))), flush=True)
         return

@@ -155,6 +155,38 @@ ssba_status ssba_forward_dense(const ssba_desc* d, const void* q, const void* k,
 ssba_status ssba_forward_topk(const ssba_desc* d, const void* q, const void* k, const void* v,
                               int32_t* index, void* scratch, void* o, void* hip_stream);
 
+/* Training forward: ssba_forward plus `lse`, fp32 [B][H][T], the natural-log
+ * log-sum-exp of each row's scaled scores (log of the softmax normaliser,
+ * log sum_j exp(scale q . k_j) over the row's visible keys), which
+ * ssba_backward needs.  bf16, head_dim 64 or 128, 8x8 or 16x16 blocks (the
+ * MFMA kernel); other shapes return SSBA_ERR_UNSUPPORTED.  `lse` 4-byte
+ * aligned, caller-owned. */
+ssba_status ssba_forward_train(const ssba_desc* d, const void* q, const void* k, const void* v,
+                               const int32_t* index, void* o, float* lse, void* hip_stream);
+
+/* Device bytes of the scratch ssba_backward needs (256-byte aligned buffer):
+ * fp32 [B][H][T] twice (the log-sum-exp in log2 units and rowsum(dO * O)) and
+ * a 64-bit mask of kept blocks per query block, [B][H][T_b]; each region
+ * rounded up to 256 bytes. */
+ssba_status ssba_backward_workspace_size(const ssba_desc* d, size_t* scratch_bytes);
+
+/* Backward of the SSBA attention with the gate held fixed (the kept lists
+ * carry no gradient): given Q, K, V, the forward output O and its lse (from
+ * ssba_forward_train with the same descriptor and index) and the upstream
+ * gradient dout (dO), writes
+ *   dq = scale dS K,  dk = scale dS^T Q,  dv = P^T dO,
+ * with P = softmax(scale Q K^T + mask) recomputed from lse, dP = dO V^T and
+ * dS = P * (dP - rowsum(dO * O)).  The mask is that of ssba_forward: image
+ * queries see their kept blocks and the text keys, text queries see every
+ * key.  All tensors bf16 with the descriptor's layout (dq, dk, dv written in
+ * full, every row); products on MFMA with fp32 accumulation, P and dS rounded
+ * to bf16 before their products.  bf16, 8x8 blocks, head_dim 64 or 128, at
+ * most 64 blocks; other shapes return SSBA_ERR_UNSUPPORTED.  The gate fields
+ * of the descriptor are not used. */
+ssba_status ssba_backward(const ssba_desc* d, const void* q, const void* k, const void* v, const void* o,
+                          const void* dout, const float* lse, const int32_t* index, void* dq, void* dk,
+                          void* dv, void* scratch, void* hip_stream);
+
 /* One layer of a stack run by ssba_forward_layers. */
 typedef struct ssba_layer {
   const void* q;    /* this layer's Q, K, V and output O (layout of the descriptor) */

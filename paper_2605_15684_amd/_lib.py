@@ -29,7 +29,8 @@ GATE_TOPK_SHARED = 3
 EXPORTS = ("ssba_abi_version", "ssba_status_str", "ssba_workspace_size", "ssba_build_index",
            "ssba_forward", "ssba_forward_dense", "ssba_read_device_status",
            "ssba_forward_kernel", "ssba_forward_topk", "ssba_layers_workspace_size",
-           "ssba_forward_layers", "ssba_haar_dwt", "ssba_haar_iwt", "ssba_haar_kernel_name")
+           "ssba_forward_layers", "ssba_haar_dwt", "ssba_haar_iwt", "ssba_haar_kernel_name",
+           "ssba_forward_train", "ssba_backward_workspace_size", "ssba_backward")
 
 
 class SsbaDesc(ctypes.Structure):
@@ -103,6 +104,12 @@ def load(path: str = None) -> ctypes.CDLL:
     lib.ssba_layers_workspace_size.argtypes = [dp, ctypes.c_int, ctypes.POINTER(sz), ctypes.POINTER(sz)]
     lib.ssba_forward_layers.restype = ctypes.c_int
     lib.ssba_forward_layers.argtypes = [dp, ctypes.POINTER(SsbaLayer), ctypes.c_int, vp, vp, vp]
+    lib.ssba_forward_train.restype = ctypes.c_int
+    lib.ssba_forward_train.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp]
+    lib.ssba_backward_workspace_size.restype = ctypes.c_int
+    lib.ssba_backward_workspace_size.argtypes = [dp, ctypes.POINTER(sz)]
+    lib.ssba_backward.restype = ctypes.c_int
+    lib.ssba_backward.argtypes = [dp] + [vp] * 12
     hp = ctypes.POINTER(HaarDesc)
     lib.ssba_haar_dwt.restype = ctypes.c_int
     lib.ssba_haar_dwt.argtypes = [hp, vp, ctypes.POINTER(vp), vp]
@@ -191,3 +198,17 @@ def haar_iwt(desc, level_ptrs, residual_ptrs, x_ptr, stream) -> int:
 def haar_kernel_name(desc, inverse: bool):
     name = load().ssba_haar_kernel_name(ctypes.byref(desc), 1 if inverse else 0)
     return None if name is None else name.decode()
+
+
+def forward_train(desc, q_ptr, k_ptr, v_ptr, index_ptr, o_ptr, lse_ptr, stream) -> int:
+    return load().ssba_forward_train(ctypes.byref(desc), q_ptr, k_ptr, v_ptr, index_ptr, o_ptr, lse_ptr, stream)
+
+
+def backward_workspace_size(desc) -> int:
+    sb = ctypes.c_size_t(0)
+    check(load().ssba_backward_workspace_size(ctypes.byref(desc), ctypes.byref(sb)), "ssba_backward_workspace_size")
+    return sb.value
+
+
+def backward(desc, q, k, v, o, dout, lse, index, dq, dk, dv, scratch, stream) -> int:
+    return load().ssba_backward(ctypes.byref(desc), q, k, v, o, dout, lse, index, dq, dk, dv, scratch, stream)

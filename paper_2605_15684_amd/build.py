@@ -28,6 +28,7 @@ SOURCES = {
     # default accumulation-register form costs a copy per element.
     "ssba_attn_mfma.hip": ["-ffp-contract=off", "-mllvm", "-amdgpu-mfma-vgpr-form"],
     "ssba_haar.hip": ["-ffp-contract=off"],
+    "ssba_bwd.hip": [],
 }
 
 COMMON = [

@@ -112,6 +112,24 @@ size_t scratch_bytes_of(const ssba_desc* d, const Shape& s) {
   return flags_offset_of(d, s) + (size_t)4 * d->batch * d->heads * s.n_tiles;
 }
 
+// Backward scratch: lse2 and D ([B][H][T] fp32 each), then each query
+// block's kept blocks as a 64-bit mask ([B][H][T_b]); every region 256-byte
+// aligned.
+struct BwdScratch {
+  size_t lse2, delta, kmask, total;
+};
+
+BwdScratch bwd_scratch(const ssba_desc* d, const Shape& s) {
+  auto up = [](size_t x) { return (x + 255) / 256 * 256; };
+  const size_t rows = (size_t)d->batch * d->heads * s.seq;
+  BwdScratch w;
+  w.lse2 = 0;
+  w.delta = up(4 * rows);
+  w.kmask = w.delta + up(4 * rows);
+  w.total = w.kmask + up((size_t)8 * d->batch * d->heads * s.n_tiles);
+  return w;
+}
+
 // Per-layer scratch slices of the layer driver start 256-byte aligned.
 size_t layer_scratch_stride(const ssba_desc* d, const Shape& s) {
   return (scratch_bytes_of(d, s) + 255) / 256 * 256;
@@ -300,6 +318,78 @@ ssba_status ssba_forward(const ssba_desc* d, const void* q, const void* k, const
 ssba_status ssba_forward_dense(const ssba_desc* d, const void* q, const void* k, const void* v,
                                void* o, void* stream) {
   return run_attention(d, q, k, v, nullptr, o, stream, true);
+}
+
+ssba_status ssba_forward_train(const ssba_desc* d, const void* q, const void* k, const void* v,
+                               const int32_t* index, void* o, float* lse, void* stream) {
+  Shape s;
+  const ssba_status st = check_desc(d, &s, false);
+  if (st != SSBA_OK) return st;
+  if (d->dtype != SSBA_DT_BF16 ||
+      !ssba::mfma_supported(d->head_dim, d->tile, false, s.n_tiles, s.seq, (int64_t)s.seq * s.st))
+    return SSBA_ERR_UNSUPPORTED;
+  if (!q || !k || !v || !o || !index || !lse) return SSBA_ERR_ARG;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16) || !aligned(index, 4) ||
+      !aligned(lse, 4))
+    return SSBA_ERR_ARG;
+  AttnArgs a = attn_args(d, s, q, k, v, index, o, false);
+  a.lse = lse;
+  const hipError_t e = ssba::launch_attn_bf16(a, d->head_dim, d->tile, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SSBA_OK : SSBA_ERR_HIP;
+}
+
+ssba_status ssba_backward_workspace_size(const ssba_desc* d, size_t* scratch_bytes) {
+  Shape s;
+  const ssba_status st = check_desc(d, &s, false);
+  if (st != SSBA_OK) return st;
+  if (scratch_bytes) *scratch_bytes = bwd_scratch(d, s).total;
+  return SSBA_OK;
+}
+
+ssba_status ssba_backward(const ssba_desc* d, const void* q, const void* k, const void* v, const void* o,
+                          const void* dout, const float* lse, const int32_t* index, void* dq, void* dk,
+                          void* dv, void* scratch, void* stream) {
+  Shape s;
+  const ssba_status st = check_desc(d, &s, false);
+  if (st != SSBA_OK) return st;
+  if (!ssba::bwd_supported(d->head_dim, d->tile, s.n_tiles, d->dtype) ||
+      !ssba::mfma_supported(d->head_dim, d->tile, false, s.n_tiles, s.seq, (int64_t)s.seq * s.st))
+    return SSBA_ERR_UNSUPPORTED;
+  const void* t16[] = {q, k, v, o, dout, dq, dk, dv};
+  for (const void* p : t16)
+    if (!p || !aligned(p, 16)) return SSBA_ERR_ARG;
+  if (!lse || !index || !scratch || !aligned(lse, 4) || !aligned(index, 4) || !aligned(scratch, 256))
+    return SSBA_ERR_ARG;
+  const BwdScratch w = bwd_scratch(d, s);
+  ssba::BwdArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.o = o;
+  a.dout = dout;
+  a.dq = dq;
+  a.dk = dk;
+  a.dv = dv;
+  a.lse = lse;
+  char* base = static_cast<char*>(scratch);
+  a.lse2 = reinterpret_cast<float*>(base + w.lse2);
+  a.delta = reinterpret_cast<float*>(base + w.delta);
+  a.kmask = reinterpret_cast<unsigned long long*>(base + w.kmask);
+  a.index = index;
+  a.sb = s.sb;
+  a.sh = s.sh;
+  a.st = s.st;
+  a.batch = d->batch;
+  a.heads = d->heads;
+  a.seq = s.seq;
+  a.n_tiles = s.n_tiles;
+  a.f = s.f;
+  const float scale = d->softmax_scale > 0.f ? d->softmax_scale : 1.0f / std::sqrt((float)d->head_dim);
+  a.scale = scale;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  const hipError_t e = ssba::launch_backward(a, d->head_dim, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SSBA_OK : SSBA_ERR_HIP;
 }
 
 ssba_status ssba_layers_workspace_size(const ssba_desc* d, int n_layers, size_t* index_bytes,

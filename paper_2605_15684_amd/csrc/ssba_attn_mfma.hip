@@ -583,6 +583,7 @@ k_attn_mfma(AttnArgs a) {
     const float mm = fmaxf(m_run, m1);
     const float a0 = __builtin_amdgcn_exp2f(m_run - mm), a1 = __builtin_amdgcn_exp2f(m1 - mm);
     l_run = l_run * a0 + l1 * a1;
+    m_run = mm;   // l_run is now relative to the merged max
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
@@ -592,6 +593,8 @@ k_attn_mfma(AttnArgs a) {
   // Epilogue: O = O^T / l, 4 consecutive channels per store.
   const float l = swap_sum(l_run);
   const float inv = l > 0.f ? 1.0f / l : 0.f;
+  if (a.lse && qrow >= 0 && hw == 0)   // m and l are in units of log2: convert to natural log
+    a.lse[(int64_t)bh * a.seq + qrow] = (m_run + __builtin_amdgcn_logf(l)) * 0.69314718055994531f;
   if (qrow >= 0) {
     u16* orow = obase + qrow * st;
 #pragma unroll

@@ -1,0 +1,581 @@
+// SSBA attention backward (gradients of Algorithm 1's attend step with the
+// gate held fixed, i.e. through the same kept lists): for the masked softmax
+// P = softmax(scale Q K^T + mask) and the upstream gradient dO,
+//   D = rowsum(dO * O),  dV = P^T dO,  dP = dO V^T,  dS = P * (dP - D),
+//   dQ = scale dS K,  dK = scale dS^T Q,
+// with P recomputed from the forward's per-row log-sum-exp.
+//
+// Kernels (bf16 tensors, 8x8 blocks, head_dim 64 / 128, at most 64 blocks):
+//   k_bwd_dq        query side, like the forward: a 64-query group forms D and
+//                   the log-sum-exp in log2 units of its rows and the 64-bit
+//                   mask of its kept blocks (all stored for the key side),
+//                   then walks its kept key blocks and the text keys;
+//   k_bwd_dkdv      key side: a 64-key group reads the head's masks, ballots
+//                   the query blocks that kept it (ascending) and walks them
+//                   plus the text queries (text key groups: every query).
+// Both main kernels use v_mfma_f32_32x32x16_bf16 with four waves per group:
+// two row halves of the group x two streams over each 64-row chunk of the
+// other side, merged once at the end.  Chunks are copied into LDS with
+// buffer_load ... lds in a row layout whose swizzle is conflict-free both for
+// 16-byte row reads and for ds_read_b64_tr_b16 transposed reads, so one copy
+// serves both operand orientations.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "ssba_common.h"
+
+namespace ssba {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx2 __attribute__((ext_vector_type(2)));
+typedef float floatx8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef uint16_t u16;
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+typedef __attribute__((address_space(3))) void lds_void;
+
+constexpr int kWaitVm0 = 0x0F70;          // s_waitcnt: every vector memory operation done
+constexpr int kRawBufferFlags = 0x00020000;
+constexpr float kLog2e = 1.4426950408889634f;
+
+template <int D>
+struct BShape {
+  static constexpr int CPR = D / 8;            // 16-byte chunks per row
+  static constexpr int ROWB = 2 * D;           // bytes per row
+  static constexpr int KPI = 1024 / ROWB;      // rows per copy instruction
+  static constexpr int NI = 32 / KPI;          // copy instructions per 32-row half
+  static constexpr int NIW = NI / 2;           // ... per wave (two waves share a half)
+  static constexpr int HALF = 32 * ROWB;       // bytes of a half tile
+  static constexpr int NKS = D / 16;           // 16-channel steps of a row product
+  static constexpr int NDB = D / 32;           // 32-channel output tiles
+};
+
+// Physical 16-byte chunk of logical chunk c in row k (0..31) of a half tile.
+// Chosen (by exhaustive search over XOR maps of the row bits) so that both the
+// 16-byte row reads of 32 rows at one chunk and the transposed 8-byte reads of
+// four rows x four channel quads hit distinct banks.
+template <int D>
+__device__ __forceinline__ int swz(int k, int c) {
+  if constexpr (D == 64)
+    return c ^ ((4 * ((k >> 1) & 1)) ^ ((k >> 2) & 1) ^ (2 * ((k >> 3) & 1)));
+  else
+    return c ^ ((4 * (k & 1)) ^ (8 * ((k >> 1) & 1)) ^ ((k >> 2) & 1) ^ (2 * ((k >> 3) & 1)));
+}
+
+__device__ __forceinline__ uint32_t pack2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2{lo, hi}, bf16x2));
+}
+
+// Row operand of a 32x32x16 product from a half tile: row l % 32, logical
+// chunk 2 ks + l / 32 (eight consecutive channels).
+template <int D>
+__device__ __forceinline__ bf16x8 row_frag(const char* half, int lane, int ks) {
+  const int k = lane & 31, c = 2 * ks + (lane >> 5);
+  return *reinterpret_cast<const bf16x8*>(half + k * BShape<D>::ROWB + 16 * swz<D>(k, c));
+}
+
+// Transposed operand (channels x rows) of a 32x32x16 product from a half
+// tile: 32 channels 32 db + (lane % 32) ... as the hardware transposing read
+// lays them out, over rows 16 ks + 8 (e / 4) + 4 (lane / 32) + e % 4.
+template <int D>
+__device__ __forceinline__ s16x8 tr_frag(const char* half, int lane, int ks, int db) {
+  const int G = lane >> 4, li = lane & 15, hw = lane >> 5;
+  const int ch = 32 * db + 16 * (G & 1) + 4 * (li & 3);
+  const int c = ch >> 3, off = 2 * (ch & 7);
+  s16x4 x[2];
+#pragma unroll
+  for (int rr = 0; rr < 2; ++rr) {
+    const int k = 16 * ks + 8 * rr + 4 * hw + (li >> 2);
+    x[rr] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_s16x4*)(half + k * BShape<D>::ROWB + 16 * swz<D>(k, c) + off));
+  }
+  return s16x8{x[0][0], x[0][1], x[0][2], x[0][3], x[1][0], x[1][1], x[1][2], x[1][3]};
+}
+
+// B operand from registers: P^T / dS^T rows 16 ks + 8 (e / 4) + 4 (lane / 32) + e % 4.
+__device__ __forceinline__ bf16x8 packed_frag(const uint32_t (&pk)[8], int ks) {
+  return __builtin_bit_cast(bf16x8, make_uint4(pk[4 * ks], pk[4 * ks + 1], pk[4 * ks + 2], pk[4 * ks + 3]));
+}
+
+// Sum of v over lanes l and l ^ 32 (the swap returns both halves' values).
+__device__ __forceinline__ float swap_sum(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Sequence row of row s (0..63) of chunk `src`: an image block (src >= 0) of
+// the shifted frame, or text chunk -1 - src (rows 64 c ..), clamped into the
+// text rows; `valid` is false for clamped rows.
+__device__ __forceinline__ int chunk_row(const Frame& f, int src, int s, bool& valid) {
+  if (src >= 0) {
+    valid = true;
+    return frame_row(f, src, s);
+  }
+  const int r = 64 * (-1 - src) + s;
+  valid = r < f.n_text;
+  return valid ? r : f.n_text - 1;
+}
+
+// This wave's share (NIW instructions) of the copy of half `hf` of chunk
+// `src` from the tensor behind `rs` into `dst` (the half tile's LDS base).
+// Two waves share a half: sub = 0 / 1 selects the instructions.
+template <int D>
+__device__ __forceinline__ void copy_half(const __amdgpu_buffer_rsrc_t& rs, const Frame& f, int src, int hf,
+                                          int sub, int st, char* dst, int lane) {
+  using S = BShape<D>;
+  const int kin = lane / S::CPR, pch = lane % S::CPR;
+#pragma unroll
+  for (int mm = 0; mm < S::NIW; ++mm) {
+    const int m = S::NIW * sub + mm;
+    const int k = S::KPI * m + kin;               // row within the half
+    bool valid;
+    const int row = chunk_row(f, src, 32 * hf + k, valid);
+    const unsigned voff = 2u * (unsigned)row * (unsigned)st + 16u * (unsigned)swz<D>(k, pch);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(dst + 1024 * m), 16, voff, 0, 0, 0);
+  }
+}
+
+// One float per chunk row (the log-sum-exp or D of the 64 rows) into LDS.
+__device__ __forceinline__ void copy_rowvals(const __amdgpu_buffer_rsrc_t& rs, const Frame& f, int src,
+                                             float* dst, int lane) {
+  bool valid;
+  const int row = chunk_row(f, src, lane, valid);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)dst, 4, 4u * (unsigned)row, 0, 0, 0);
+}
+
+// Workgroup -> (b, h, group): every (b, h) owns n_text_groups text groups and
+// n_tiles image groups; with a head count divisible by 8 each XCD (hardware
+// ids go round-robin over the 8) gets whole heads, text groups first.
+__device__ __forceinline__ void group_of(const BwdArgs& a, int& bh, int& r) {
+  const int bid = blockIdx.x, nbh = a.batch * a.heads, gpb = a.n_text_groups + a.n_tiles;
+  if ((nbh & 7) == 0) {
+    const int xcd = bid & 7, s = bid >> 3, hpx = nbh >> 3;
+    const int nt = a.n_text_groups;
+    if (s < hpx * nt) {
+      bh = xcd * hpx + s / nt;
+      r = s % nt;
+    } else {
+      const int s2 = s - hpx * nt;
+      bh = xcd * hpx + s2 / a.n_tiles;
+      r = nt + s2 % a.n_tiles;
+    }
+  } else {
+    bh = bid / gpb;
+    r = bid - bh * gpb;
+  }
+}
+
+// --------------------------------------------------------------------------
+// dQ: one workgroup per 64-query group.  Wave w: query half qh = w % 2, key
+// stream sk = w / 2 (keys 32 sk .. 32 sk + 31 of every 64-key chunk).
+// Per chunk: S^T = K Q'^T - lse2 (Q' = Q scale log2 e rounded to bf16, as in
+// the forward), P^T = exp2(S^T), dP^T = V dO^T, dS^T = P^T (dP^T - D),
+// dQ^T += K^T dS^T.
+// --------------------------------------------------------------------------
+template <int D>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k_bwd_dq(BwdArgs a) {
+  using S = BShape<D>;
+  constexpr int HALF = S::HALF, NKS = S::NKS, NDB = S::NDB;
+  __shared__ __attribute__((aligned(16))) char kbuf[2][2 * HALF];   // [buffer][stream half]
+  __shared__ __attribute__((aligned(16))) char vbuf[2][2 * HALF];
+  int bh, r;
+  group_of(a, bh, r);
+  const int b = bh / a.heads, h = bh - b * a.heads;
+  const int64_t off = (int64_t)b * a.sb + (int64_t)h * a.sh;
+  const u16* qbase = static_cast<const u16*>(a.q) + off;
+  const u16* kbase = static_cast<const u16*>(a.k) + off;
+  const u16* vbase = static_cast<const u16*>(a.v) + off;
+  const u16* gbase = static_cast<const u16*>(a.dout) + off;
+  const int st = (int)a.st;
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int qh = w & 1, sk = w >> 1, hw = lane >> 5, l32 = lane & 31;
+
+  // This lane's query row and the chunk plan.
+  const bool text_group = r < a.n_text_groups;
+  int qrow;
+  if (text_group) {
+    const int q = 64 * r + 32 * qh + l32;
+    qrow = q < a.f.n_text ? q : -1;
+  } else {
+    qrow = frame_row(a.f, r - a.n_text_groups, 32 * qh + l32);
+  }
+  const int qr = max(qrow, 0);
+  // Chunks: text groups see every key (the text chunks, then every image
+  // block in block order); image groups their kept blocks, then the text.
+  const int n_txt = (a.f.n_text + 63) / 64;
+  int n_img, listv = -1;
+  if (text_group) {
+    n_img = a.n_tiles;
+  } else {
+    const int32_t* list = a.index + ((int64_t)bh * a.n_tiles + (r - a.n_text_groups)) * (a.n_tiles + 1);
+    const int raw = list[0];
+    const int ent = lane < a.n_tiles ? list[1 + lane] : 0;
+    n_img = min(max(raw, 0), a.n_tiles);
+    listv = lane < n_img ? ent : -1;
+    if ((unsigned)listv >= (unsigned)a.n_tiles) listv = -1;
+  }
+  const int n = n_img + n_txt;
+  // The kept blocks of an image group as a 64-bit mask, for the key side.
+  __shared__ unsigned long long kept_mask;
+  if (threadIdx.x == 0) kept_mask = 0ull;
+  __syncthreads();
+  if (!text_group && w == 0 && listv >= 0) atomicOr(&kept_mask, 1ull << listv);
+  // Chunk c -> source: image blocks first (block id, -1000000 marks an
+  // invalid id), then text chunk -1 - t.
+  auto src_of = [&](int c) {
+    if (c < n_img) {
+      if (text_group) return c;
+      const int j = __builtin_amdgcn_readlane(listv, c);
+      return j >= 0 ? j : -1000000;   // invalid id: masked (rows clamped to text row 0 / block 0)
+    }
+    return -1 - (c - n_img);
+  };
+
+  // Q' (scaled, rounded) and dO as B operands, lse2 and D of the lane's query.
+  bf16x8 qf[NKS], gf[NKS];
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) {
+    const bf16x8 raw = *reinterpret_cast<const bf16x8*>(qbase + (int64_t)qr * st + 16 * ks + 8 * hw);
+    qf[ks] = __builtin_convertvector(__builtin_convertvector(raw, floatx8) * a.scale_log2, bf16x8);
+    gf[ks] = *reinterpret_cast<const bf16x8*>(gbase + (int64_t)qr * st + 16 * ks + 8 * hw);
+  }
+  // D = rowsum(dO * O) of the lane's query (its 8 NKS channels here, the
+  // other half in lane ^ 32) and the log-sum-exp in log2 units; both are
+  // written for the key-side kernel, which runs after this one.
+  const int64_t rowid = (int64_t)bh * a.seq + qr;
+  const float lse2 = a.lse[rowid] * kLog2e;
+  float dlt;
+  {
+    const u16* obase = static_cast<const u16*>(a.o) + off;
+    float part = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      const uint4 x = *reinterpret_cast<const uint4*>(obase + (int64_t)qr * st + 16 * ks + 8 * hw);
+      const uint4 y = __builtin_bit_cast(uint4, gf[ks]);
+      const uint32_t xs[4] = {x.x, x.y, x.z, x.w}, ys[4] = {y.x, y.y, y.z, y.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        part += __uint_as_float(xs[e] << 16) * __uint_as_float(ys[e] << 16);
+        part += __uint_as_float(xs[e] & 0xFFFF0000u) * __uint_as_float(ys[e] & 0xFFFF0000u);
+      }
+    }
+    dlt = swap_sum(part);
+  }
+  if (sk == 0 && hw == 0 && qrow >= 0) {
+    a.delta[rowid] = dlt;
+    a.lse2[rowid] = lse2;
+  }
+  floatx16 negl;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) negl[e] = -lse2;
+
+  const unsigned slice_bytes = 2u * (unsigned)((a.seq - 1) * st + D);
+  const __amdgpu_buffer_rsrc_t rk =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<u16*>(kbase), (short)0, (int)slice_bytes, kRawBufferFlags);
+  const __amdgpu_buffer_rsrc_t rv =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<u16*>(vbase), (short)0, (int)slice_bytes, kRawBufferFlags);
+
+  auto issue = [&](int c, int buf) {
+    const int src = src_of(c);
+    const int s2 = src == -1000000 ? 0 : src;
+    copy_half<D>(rk, a.f, s2, sk, qh, st, kbuf[buf] + HALF * sk, lane);
+    copy_half<D>(rv, a.f, s2, sk, qh, st, vbuf[buf] + HALF * sk, lane);
+  };
+
+  floatx16 acc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) acc[db] = floatx16{};
+
+  if (n > 0) issue(0, 0);
+  __builtin_amdgcn_s_waitcnt(kWaitVm0);
+  __syncthreads();
+  if (!text_group && threadIdx.x == 0) a.kmask[(int64_t)bh * a.n_tiles + (r - a.n_text_groups)] = kept_mask;
+  for (int c = 0; c < n; ++c) {
+    const int buf = c & 1;
+    if (c + 1 < n) issue(c + 1, buf ^ 1);
+    const char* kt = kbuf[buf] + HALF * sk;
+    const char* vt = vbuf[buf] + HALF * sk;
+    // Valid keys of this stream's half: text chunks end at n_text.
+    const int src = src_of(c);
+    int lo = 0, hi = 32;
+    if (src == -1000000) {
+      hi = 0;
+    } else if (src < 0) {
+      const int base = 64 * (-1 - src) + 32 * sk;
+      hi = min(max(a.f.n_text - base, 0), 32);
+    }
+    floatx16 sc = negl, dp = floatx16{};
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<D>(kt, lane, ks), qf[ks], sc, 0, 0, 0);
+      dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<D>(vt, lane, ks), gf[ks], dp, 0, 0, 0);
+    }
+    uint32_t pk[8];
+#pragma unroll
+    for (int rr = 0; rr < 16; rr += 2) {
+      float ds[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int key = 8 * ((rr + u) >> 2) + 4 * hw + ((rr + u) & 3);
+        const float p = (key >= lo && key < hi) ? __builtin_amdgcn_exp2f(sc[rr + u]) : 0.f;
+        ds[u] = p * (dp[rr + u] - dlt);
+      }
+      pk[rr >> 1] = pack2(ds[0], ds[1]);
+    }
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const bf16x8 pb = packed_frag(pk, ks);
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, tr_frag<D>(kt, lane, ks, db)),
+                                                         pb, acc[db], 0, 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(kWaitVm0);
+    __syncthreads();
+  }
+
+  // Merge the two key streams through LDS (the K buffers are free now).
+  float* xo = reinterpret_cast<float*>(kbuf[0]) + (size_t)qh * 16 * NDB * 64;
+  static_assert(2 * 16 * NDB * 64 * 4 <= 2 * 2 * HALF, "merge area fits the K buffers");
+  if (sk == 1) {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) xo[(16 * db + j) * 64 + lane] = acc[db][j];
+  }
+  __syncthreads();
+  if (sk == 1 || qrow < 0) return;
+  u16* orow = static_cast<u16*>(a.dq) + off + (int64_t)qrow * st;
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = (acc[db][4 * j + e] + xo[(16 * db + 4 * j + e) * 64 + lane]) * a.scale;
+      *reinterpret_cast<uint2*>(orow + 32 * db + 8 * j + 4 * hw) = make_uint2(pack2(v[0], v[1]), pack2(v[2], v[3]));
+    }
+}
+
+// --------------------------------------------------------------------------
+// dK, dV: one workgroup per 64-key group.  Wave w: key half kh = w % 2, query
+// stream qs = w / 2 (queries 32 qs .. 32 qs + 31 of every 64-query chunk).
+// Per chunk: S = Q K^T (rows = queries), P = exp2(S scale log2 e - lse2),
+// dV^T += dO^T P, dP = dO V^T, dS = P (dP - D), dK^T += Q^T dS.
+// --------------------------------------------------------------------------
+template <int D>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 64 ? 2 : 1))) k_bwd_dkdv(BwdArgs a) {
+  using S = BShape<D>;
+  constexpr int HALF = S::HALF, NKS = S::NKS, NDB = S::NDB;
+  __shared__ __attribute__((aligned(16))) char qbuf[2][2 * HALF];   // [buffer][query half]
+  __shared__ __attribute__((aligned(16))) char gbuf[2][2 * HALF];   // dO
+  __shared__ __attribute__((aligned(16))) float lbuf[2][64];         // lse2 of the chunk's rows
+  __shared__ __attribute__((aligned(16))) float dbuf[2][64];         // D of the chunk's rows
+  int bh, r;
+  group_of(a, bh, r);
+  const int b = bh / a.heads, h = bh - b * a.heads;
+  const int64_t off = (int64_t)b * a.sb + (int64_t)h * a.sh;
+  const u16* qbase = static_cast<const u16*>(a.q) + off;
+  const u16* kbase = static_cast<const u16*>(a.k) + off;
+  const u16* vbase = static_cast<const u16*>(a.v) + off;
+  const u16* gbase = static_cast<const u16*>(a.dout) + off;
+  const int st = (int)a.st;
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int kh = w & 1, qs = w >> 1, hw = lane >> 5, l32 = lane & 31;
+
+  // This lane's key row.
+  const bool text_group = r < a.n_text_groups;
+  int krow;
+  if (text_group) {
+    const int kk = 64 * r + 32 * kh + l32;
+    krow = kk < a.f.n_text ? kk : -1;
+  } else {
+    krow = frame_row(a.f, r - a.n_text_groups, 32 * kh + l32);
+  }
+  const int kr = max(krow, 0);
+  // Query chunks: the query blocks that kept this key block (text key
+  // groups: every block), then the text query chunks.
+  const int n_txt = (a.f.n_text + 63) / 64;
+  int n_img;
+  uint64_t members = 0;   // bit i: query block i kept this key block
+  if (text_group) {
+    n_img = a.n_tiles;
+  } else {
+    const int j = r - a.n_text_groups;
+    const uint64_t m = lane < a.n_tiles ? a.kmask[(int64_t)bh * a.n_tiles + lane] : 0ull;
+    members = __ballot(((m >> j) & 1ull) != 0ull);
+    n_img = __popcll(members);
+  }
+  const int n = n_img + n_txt;
+  // Sources in chunk order: the member query blocks ascending (text key
+  // groups: every block), then text chunk -1 - t.  Taken once each, when the
+  // chunk's copy is issued.
+  uint64_t rest = members;
+  int next_blk = 0, next_txt = 0;
+  auto pop_src = [&]() {
+    if (text_group ? next_blk < a.n_tiles : rest != 0ull) {
+      int s2;
+      if (text_group) {
+        s2 = next_blk++;
+      } else {
+        s2 = (int)__builtin_ctzll(rest);
+        rest &= rest - 1ull;
+      }
+      return s2;
+    }
+    return -1 - next_txt++;
+  };
+
+  // K and V rows of the lane's key as B operands (lane = key column).
+  bf16x8 kf[NKS], vf[NKS];
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) {
+    kf[ks] = *reinterpret_cast<const bf16x8*>(kbase + (int64_t)kr * st + 16 * ks + 8 * hw);
+    vf[ks] = *reinterpret_cast<const bf16x8*>(vbase + (int64_t)kr * st + 16 * ks + 8 * hw);
+  }
+
+  const unsigned slice_bytes = 2u * (unsigned)((a.seq - 1) * st + D);
+  const __amdgpu_buffer_rsrc_t rq =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<u16*>(qbase), (short)0, (int)slice_bytes, kRawBufferFlags);
+  const __amdgpu_buffer_rsrc_t rg =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<u16*>(gbase), (short)0, (int)slice_bytes, kRawBufferFlags);
+  const __amdgpu_buffer_rsrc_t rl = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(a.lse2 + (int64_t)bh * a.seq), (short)0, 4 * a.seq, kRawBufferFlags);
+  const __amdgpu_buffer_rsrc_t rdl = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(a.delta + (int64_t)bh * a.seq), (short)0, 4 * a.seq, kRawBufferFlags);
+
+  auto issue = [&](int src, int buf) {
+    copy_half<D>(rq, a.f, src, qs, kh, st, qbuf[buf] + HALF * qs, lane);
+    copy_half<D>(rg, a.f, src, qs, kh, st, gbuf[buf] + HALF * qs, lane);
+    if (w == 0) copy_rowvals(rl, a.f, src, lbuf[buf], lane);
+    if (w == 1) copy_rowvals(rdl, a.f, src, dbuf[buf], lane);
+  };
+
+  floatx16 dk[NDB], dv[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) {
+    dk[db] = floatx16{};
+    dv[db] = floatx16{};
+  }
+
+  int src = n > 0 ? pop_src() : 0;
+  if (n > 0) issue(src, 0);
+  __builtin_amdgcn_s_waitcnt(kWaitVm0);
+  __syncthreads();
+  for (int c = 0; c < n; ++c) {
+    const int buf = c & 1;
+    const int nsrc = c + 1 < n ? pop_src() : 0;
+    if (c + 1 < n) issue(nsrc, buf ^ 1);
+    const char* qt = qbuf[buf] + HALF * qs;
+    const char* gt = gbuf[buf] + HALF * qs;
+    // Valid queries of this stream's half (text chunks end at n_text).
+    int hi = 32;
+    if (src < 0) hi = min(max(a.f.n_text - (64 * (-1 - src) + 32 * qs), 0), 32);
+    // Row values: element e of the lane's tile is query 8 (e / 4) + 4 hw + e % 4.
+    float nl[16], dl[16];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const float4 x = *reinterpret_cast<const float4*>(&lbuf[buf][32 * qs + 8 * g + 4 * hw]);
+      const float4 y = *reinterpret_cast<const float4*>(&dbuf[buf][32 * qs + 8 * g + 4 * hw]);
+      nl[4 * g] = -x.x; nl[4 * g + 1] = -x.y; nl[4 * g + 2] = -x.z; nl[4 * g + 3] = -x.w;
+      dl[4 * g] = y.x; dl[4 * g + 1] = y.y; dl[4 * g + 2] = y.z; dl[4 * g + 3] = y.w;
+    }
+    floatx16 sc = floatx16{}, dp = floatx16{};
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<D>(qt, lane, ks), kf[ks], sc, 0, 0, 0);
+      dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<D>(gt, lane, ks), vf[ks], dp, 0, 0, 0);
+    }
+    // The chunk's rows carry Q itself: the product is scaled here.
+    uint32_t pp[8], pd[8];
+#pragma unroll
+    for (int rr = 0; rr < 16; rr += 2) {
+      float p[2], ds[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int q = 8 * ((rr + u) >> 2) + 4 * hw + ((rr + u) & 3);
+        p[u] = q < hi ? __builtin_amdgcn_exp2f(__builtin_fmaf(sc[rr + u], a.scale_log2, nl[rr + u])) : 0.f;
+        ds[u] = p[u] * (dp[rr + u] - dl[rr + u]);
+      }
+      pp[rr >> 1] = pack2(p[0], p[1]);
+      pd[rr >> 1] = pack2(ds[0], ds[1]);
+    }
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const bf16x8 pb = packed_frag(pp, ks), db8 = packed_frag(pd, ks);
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        dv[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, tr_frag<D>(gt, lane, ks, db)),
+                                                        pb, dv[db], 0, 0, 0);
+        dk[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, tr_frag<D>(qt, lane, ks, db)),
+                                                        db8, dk[db], 0, 0, 0);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(kWaitVm0);
+    __syncthreads();
+    src = nsrc;
+  }
+
+  // Merge the two query streams through LDS (the Q / dO buffers are free).
+  static_assert(2 * 16 * NDB * 64 * 4 <= 2 * 2 * HALF, "merge area fits one buffer pair");
+  float* xk = reinterpret_cast<float*>(qbuf[0]) + (size_t)kh * 16 * NDB * 64;
+  float* xv = reinterpret_cast<float*>(gbuf[0]) + (size_t)kh * 16 * NDB * 64;
+  if (qs == 1) {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        xk[(16 * db + j) * 64 + lane] = dk[db][j];
+        xv[(16 * db + j) * 64 + lane] = dv[db][j];
+      }
+  }
+  __syncthreads();
+  if (qs == 1 || krow < 0) return;
+  u16* krow_k = static_cast<u16*>(a.dk) + off + (int64_t)krow * st;
+  u16* krow_v = static_cast<u16*>(a.dv) + off + (int64_t)krow * st;
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float vk[4], vv[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int x = (16 * db + 4 * j + e) * 64 + lane;
+        vk[e] = (dk[db][4 * j + e] + xk[x]) * a.scale;
+        vv[e] = dv[db][4 * j + e] + xv[x];
+      }
+      *reinterpret_cast<uint2*>(krow_k + 32 * db + 8 * j + 4 * hw) = make_uint2(pack2(vk[0], vk[1]), pack2(vk[2], vk[3]));
+      *reinterpret_cast<uint2*>(krow_v + 32 * db + 8 * j + 4 * hw) = make_uint2(pack2(vv[0], vv[1]), pack2(vv[2], vv[3]));
+    }
+}
+
+}  // namespace
+
+bool bwd_supported(int head_dim, int tile, int n_tiles, int dtype) {
+  return dtype == SSBA_DT_BF16 && (head_dim == 64 || head_dim == 128) && tile == 8 && n_tiles <= 64;
+}
+
+hipError_t launch_backward(const BwdArgs& a0, int head_dim, hipStream_t s) {
+  BwdArgs a = a0;
+  a.n_text_groups = (a.f.n_text + 63) / 64;
+  const dim3 blk(256);
+  const dim3 grid((unsigned)(a.batch * a.heads * (a.n_text_groups + a.n_tiles)));
+  if (head_dim == 64) {
+    hipLaunchKernelGGL(k_bwd_dq<64>, grid, blk, 0, s, a);
+    hipLaunchKernelGGL(k_bwd_dkdv<64>, grid, blk, 0, s, a);
+  } else {
+    hipLaunchKernelGGL(k_bwd_dq<128>, grid, blk, 0, s, a);
+    hipLaunchKernelGGL(k_bwd_dkdv<128>, grid, blk, 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace ssba

@@ -92,6 +92,9 @@ struct AttnArgs {
   const double* kb;      // [B][H][D][T_b] pooled key sums
   int32_t* index_out;    // [B][H][T_b][1 + T_b]
   int32_t* flags;        // [B][H][T_b]
+  // Optional (MFMA kernels): natural-log log-sum-exp of each row's scaled
+  // scores, [B][H][T] fp32, for the backward pass.
+  float* lse;
 };
 
 struct IndexArgs {
@@ -107,6 +110,27 @@ struct IndexArgs {
   Frame f;
 };
 
+// Everything the backward kernels need.
+struct BwdArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* o;
+  const void* dout;
+  void* dq;
+  void* dk;
+  void* dv;
+  const float* lse;      // [B][H][T] natural-log log-sum-exp from the forward
+  float* lse2;           // [B][H][T] scratch: lse * log2(e)
+  float* delta;          // [B][H][T] scratch: rowsum(dO * O)
+  const int32_t* index;  // [B][H][T_b][1 + T_b]
+  unsigned long long* kmask;  // [B][H][T_b] scratch: kept blocks of each query block as bits
+  int64_t sb, sh, st;
+  int batch, heads, seq, n_tiles, n_text_groups;
+  Frame f;
+  float scale, scale_log2;
+};
+
 // Launchers (each returns hipGetLastError() of its launch).
 hipError_t launch_pool(const IndexArgs& a, int dtype, hipStream_t s);
 hipError_t launch_gate_topk(const IndexArgs& a, hipStream_t s);
@@ -120,6 +144,9 @@ hipError_t launch_attn_f32(const AttnArgs& a, int head_dim, int tile, hipStream_
 bool mfma_supported(int head_dim, int tile, bool dense, int n_tiles, int seq, int64_t span);
 hipError_t launch_attn_mfma(const AttnArgs& a, int head_dim, int tile, hipStream_t s);
 const char* mfma_kernel_name(int head_dim, int tile, bool dense, bool gated);
+// Backward: bf16, 8x8 blocks, head_dim 64 / 128, at most 64 blocks.
+bool bwd_supported(int head_dim, int tile, int n_tiles, int dtype);
+hipError_t launch_backward(const BwdArgs& a, int head_dim, hipStream_t s);
 // Name of the kernel launch_attn_bf16 / launch_attn_f32 would run.
 const char* attn_kernel_name(const AttnArgs& a, int head_dim, int tile, int dtype);
 

@@ -21,7 +21,8 @@ from . import _lib
 _lib.load()   # fail loudly at import if the HIP library is missing
 
 __all__ = ["make_desc", "desc_for", "alloc_workspace", "build_index", "forward", "forward_dense",
-           "forward_topk", "forward_layers", "attention", "read_status", "layer_shift",
+           "forward_topk", "forward_layers", "forward_train", "backward", "attention", "read_status",
+           "layer_shift",
            "keep_from_rho", "SsbaError"]
 
 SsbaError = _lib.SsbaError
@@ -203,6 +204,36 @@ def forward_layers(layers, desc, index=None, scratch=None):
     _lib.check(_lib.forward_layers(desc, arr, index.data_ptr(), scratch.data_ptr(), _stream(dev)),
                "ssba_forward_layers")
     return index, scratch
+
+
+def forward_train(q, k, v, index, desc, out=None, lse=None):
+    """ssba_forward that also returns the per-row log-sum-exp (fp32 [B, H, T])
+    the backward needs.  Returns (out, lse)."""
+    if out is None:
+        out = torch.empty_strided(q.shape, q.stride(), dtype=q.dtype, device=q.device)
+    if lse is None:
+        lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
+    _check_tensors(desc, q, k, v, out)
+    if not (lse.is_cuda and lse.dtype == torch.float32 and lse.is_contiguous() and lse.shape == q.shape[:3]):
+        raise ValueError("lse must be a contiguous fp32 GPU tensor of shape [B, H, T]")
+    _lib.check(_lib.forward_train(desc, q.data_ptr(), k.data_ptr(), v.data_ptr(), index.data_ptr(),
+                                  out.data_ptr(), lse.data_ptr(), _stream(q.device)), "ssba_forward_train")
+    return out, lse
+
+
+def backward(q, k, v, out, dout, lse, index, desc, dq=None, dk=None, dv=None, scratch=None):
+    """Gradients (dq, dk, dv) of the SSBA attention for upstream gradient
+    `dout`, with the gate held fixed (ssba_backward)."""
+    mk = lambda t: torch.empty_strided(q.shape, q.stride(), dtype=q.dtype, device=q.device) if t is None else t
+    dq, dk, dv = mk(dq), mk(dk), mk(dv)
+    _check_tensors(desc, q, k, v, out, dout, dq, dk, dv)
+    if scratch is None:
+        sb = _lib.backward_workspace_size(desc)
+        scratch = torch.empty(((sb + 7) // 8,), dtype=torch.float64, device=q.device)
+    _lib.check(_lib.backward(desc, q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), dout.data_ptr(),
+                             lse.data_ptr(), index.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
+                             scratch.data_ptr(), _stream(q.device)), "ssba_backward")
+    return dq, dk, dv
 
 
 def read_status(desc, scratch) -> int:

@@ -238,3 +238,34 @@ def test_haar_null_and_misaligned_pointers_rejected(lib):
 def test_haar_kernel_names(lib):
     assert _lib.haar_kernel_name(_hdesc(), False) == "k_haar_dwt<unsigned short, 3>"
     assert _lib.haar_kernel_name(_hdesc(levels=1, dtype=_lib.DT_F32), True) == "k_haar_iwt<float, 1>"
+
+
+@pytest.mark.parametrize("kw", [{"tile": 16, "grid_h": 128, "grid_w": 128, "keep": 7},
+                                {"dtype": _lib.DT_F32, "tile": 4, "grid_h": 16, "grid_w": 16, "keep": 4},
+                                {"grid_h": 128, "grid_w": 128}])      # 256 blocks
+def test_backward_unsupported_shapes_rejected_before_launch(lib, kw):
+    d = _desc(**kw)
+    fake = 1 << 20
+    assert _lib.backward(d, *([fake] * 11), None) == _lib.SSBA_ERR_UNSUPPORTED
+
+
+def test_backward_arguments_rejected_before_launch(lib):
+    d = _desc()
+    fake = 1 << 20
+    args = [fake] * 11                           # q k v o dout lse index dq dk dv scratch
+    for i in range(11):
+        bad = list(args)
+        bad[i] = None
+        assert _lib.backward(d, *bad, None) == _lib.SSBA_ERR_ARG
+    bad = list(args)
+    bad[10] = fake + 16                          # scratch must be 256-byte aligned
+    assert _lib.backward(d, *bad, None) == _lib.SSBA_ERR_ARG
+    assert _lib.forward_train(d, fake, fake, fake, fake, fake, None, None) == _lib.SSBA_ERR_ARG
+    assert _lib.forward_train(_desc(dtype=_lib.DT_F32), *([fake] * 6), None) == _lib.SSBA_ERR_UNSUPPORTED
+
+
+def test_backward_workspace_size(lib):
+    d = _desc(batch=2, heads=3, n_text=10)
+    rows = 2 * 3 * (10 + 4096)
+    up = lambda x: (x + 255) // 256 * 256
+    assert _lib.backward_workspace_size(d) == 2 * up(4 * rows) + up(8 * 2 * 3 * 64)
