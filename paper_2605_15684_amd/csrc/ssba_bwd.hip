@@ -120,23 +120,64 @@ __device__ __forceinline__ int chunk_row(const Frame& f, int src, int s, bool& v
   return valid ? r : f.n_text - 1;
 }
 
-// This wave's share (NIW instructions) of the copy of half `hf` of chunk
-// `src` from the tensor behind `rs` into `dst` (the half tile's LDS base).
-// Two waves share a half: sub = 0 / 1 selects the instructions.
+// Copies of a half tile: two waves share a half, sub = 0 / 1 selecting NIW
+// of its NI copy instructions.  Lane l of instruction m fills row
+// k = KPI m + l / CPR of the half, physical chunk l % CPR, i.e. the logical
+// chunk that the swizzle puts there; zoff[mm] is that chunk's byte offset
+// (a per-lane constant).
 template <int D>
-__device__ __forceinline__ void copy_half(const __amdgpu_buffer_rsrc_t& rs, const Frame& f, int src, int hf,
-                                          int sub, int st, char* dst, int lane) {
+__device__ __forceinline__ void swizzle_offsets(int sub, int lane, unsigned (&zoff)[BShape<D>::NIW]) {
   using S = BShape<D>;
   const int kin = lane / S::CPR, pch = lane % S::CPR;
 #pragma unroll
   for (int mm = 0; mm < S::NIW; ++mm) {
-    const int m = S::NIW * sub + mm;
-    const int k = S::KPI * m + kin;               // row within the half
-    bool valid;
-    const int row = chunk_row(f, src, 32 * hf + k, valid);
-    const unsigned voff = 2u * (unsigned)row * (unsigned)st + 16u * (unsigned)swz<D>(k, pch);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(dst + 1024 * m), 16, voff, 0, 0, 0);
+    const int k = S::KPI * (S::NIW * sub + mm) + kin;
+    zoff[mm] = 16u * (unsigned)swz<D>(k, pch);   // swz is an involution on the chunk bits
   }
+}
+
+// Byte offsets, inside the (batch, head) slice, of this wave's copy
+// instructions for half `hf` of chunk `src` (an image block of 8x8 tokens,
+// or text chunk -1 - src with rows past the text clamped to its last row).
+// The block origin is found once per chunk; an instruction's rows lie in one
+// block row (KPI <= 8), so only the column depends on the lane.
+template <int D>
+__device__ __forceinline__ void copy_offsets(const Frame& f, int src, int hf, int sub, unsigned st2,
+                                             const unsigned (&zoff)[BShape<D>::NIW], int lane,
+                                             unsigned (&off)[BShape<D>::NIW]) {
+  using S = BShape<D>;
+  static_assert(S::KPI <= 8 && 8 % S::KPI == 0, "an instruction stays inside one block row");
+  const int kin = lane / S::CPR;
+  if (src >= 0) {
+    const int ty = src / f.nx, tx = src - ty * f.nx;
+    const int y0 = (ty << 3) - f.sy + 4 * hf, x0 = (tx << 3) - f.sx;
+#pragma unroll
+    for (int mm = 0; mm < S::NIW; ++mm) {
+      const int k = S::KPI * (S::NIW * sub + mm);   // first row of the instruction
+      int y = y0 + (k >> 3);
+      y += y < 0 ? f.grid_h : 0;
+      int x = x0 + (k & 7) + kin;
+      x += x < 0 ? f.grid_w : 0;
+      off[mm] = st2 * (unsigned)(f.n_text + y * f.grid_w) + st2 * (unsigned)x + zoff[mm];
+    }
+  } else {
+    const int base = 64 * (-1 - src) + 32 * hf;
+#pragma unroll
+    for (int mm = 0; mm < S::NIW; ++mm) {
+      const int row = min(base + S::KPI * (S::NIW * sub + mm) + kin, f.n_text - 1);
+      off[mm] = st2 * (unsigned)row + zoff[mm];
+    }
+  }
+}
+
+// This wave's share of the copy of a half tile from the tensor behind `rs`
+// into `dst` (the half tile's LDS base), at offsets from copy_offsets.
+template <int D>
+__device__ __forceinline__ void copy_half(const __amdgpu_buffer_rsrc_t& rs, const unsigned* off, int sub, char* dst) {
+  using S = BShape<D>;
+#pragma unroll
+  for (int mm = 0; mm < S::NIW; ++mm)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(dst + 1024 * (S::NIW * sub + mm)), 16, off[mm], 0, 0, 0);
 }
 
 // One float per chunk row (the log-sum-exp or D of the 64 rows) into LDS.
@@ -280,11 +321,14 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
   const __amdgpu_buffer_rsrc_t rv =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<u16*>(vbase), (short)0, (int)slice_bytes, kRawBufferFlags);
 
+  unsigned zoff[S::NIW];
+  swizzle_offsets<D>(qh, lane, zoff);
   auto issue = [&](int c, int buf) {
     const int src = src_of(c);
-    const int s2 = src == -1000000 ? 0 : src;
-    copy_half<D>(rk, a.f, s2, sk, qh, st, kbuf[buf] + HALF * sk, lane);
-    copy_half<D>(rv, a.f, s2, sk, qh, st, vbuf[buf] + HALF * sk, lane);
+    unsigned offs[S::NIW];
+    copy_offsets<D>(a.f, src == -1000000 ? 0 : src, sk, qh, 2u * (unsigned)st, zoff, lane, offs);
+    copy_half<D>(rk, offs, qh, kbuf[buf] + HALF * sk);
+    copy_half<D>(rv, offs, qh, vbuf[buf] + HALF * sk);
   };
 
   floatx16 acc[NDB];
@@ -315,16 +359,21 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
       sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<D>(kt, lane, ks), qf[ks], sc, 0, 0, 0);
       dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<D>(vt, lane, ks), gf[ks], dp, 0, 0, 0);
     }
+    if (lo > 0 || hi < 32) {   // rare: text tail or an invalid block id
+      int l4 = lo - 4 * hw, h4 = hi - 4 * hw;
+      asm volatile("" : "+v"(l4), "+v"(h4));
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) {
+        const int key = 8 * (rr >> 2) + (rr & 3);   // minus 4 * hw
+        if (key < l4 || key >= h4) sc[rr] = -INFINITY;   // P = 0, so dS = 0 (dP is finite)
+      }
+    }
     uint32_t pk[8];
 #pragma unroll
     for (int rr = 0; rr < 16; rr += 2) {
       float ds[2];
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int key = 8 * ((rr + u) >> 2) + 4 * hw + ((rr + u) & 3);
-        const float p = (key >= lo && key < hi) ? __builtin_amdgcn_exp2f(sc[rr + u]) : 0.f;
-        ds[u] = p * (dp[rr + u] - dlt);
-      }
+      for (int u = 0; u < 2; ++u) ds[u] = __builtin_amdgcn_exp2f(sc[rr + u]) * (dp[rr + u] - dlt);
       pk[rr >> 1] = pack2(ds[0], ds[1]);
     }
 #pragma unroll
@@ -451,9 +500,13 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
   const __amdgpu_buffer_rsrc_t rdl = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<float*>(a.delta + (int64_t)bh * a.seq), (short)0, 4 * a.seq, kRawBufferFlags);
 
+  unsigned zoff[S::NIW];
+  swizzle_offsets<D>(kh, lane, zoff);
   auto issue = [&](int src, int buf) {
-    copy_half<D>(rq, a.f, src, qs, kh, st, qbuf[buf] + HALF * qs, lane);
-    copy_half<D>(rg, a.f, src, qs, kh, st, gbuf[buf] + HALF * qs, lane);
+    unsigned offs[S::NIW];
+    copy_offsets<D>(a.f, src, qs, kh, 2u * (unsigned)st, zoff, lane, offs);
+    copy_half<D>(rq, offs, kh, qbuf[buf] + HALF * qs);
+    copy_half<D>(rg, offs, kh, gbuf[buf] + HALF * qs);
     if (w == 0) copy_rowvals(rl, a.f, src, lbuf[buf], lane);
     if (w == 1) copy_rowvals(rdl, a.f, src, dbuf[buf], lane);
   };
@@ -494,14 +547,20 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
       dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<D>(gt, lane, ks), vf[ks], dp, 0, 0, 0);
     }
     // The chunk's rows carry Q itself: the product is scaled here.
+    if (hi < 32) {   // rare: text tail
+      int h4 = hi - 4 * hw;
+      asm volatile("" : "+v"(h4));
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr)
+        if (8 * (rr >> 2) + (rr & 3) >= h4) sc[rr] = -INFINITY;   // P = 0, so dS = 0
+    }
     uint32_t pp[8], pd[8];
 #pragma unroll
     for (int rr = 0; rr < 16; rr += 2) {
       float p[2], ds[2];
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        const int q = 8 * ((rr + u) >> 2) + 4 * hw + ((rr + u) & 3);
-        p[u] = q < hi ? __builtin_amdgcn_exp2f(__builtin_fmaf(sc[rr + u], a.scale_log2, nl[rr + u])) : 0.f;
+        p[u] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[rr + u], a.scale_log2, nl[rr + u]));
         ds[u] = p[u] * (dp[rr + u] - dl[rr + u]);
       }
       pp[rr >> 1] = pack2(p[0], p[1]);
