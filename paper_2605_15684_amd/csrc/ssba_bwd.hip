@@ -221,8 +221,13 @@ template <int D>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k_bwd_dq(BwdArgs a) {
   using S = BShape<D>;
   constexpr int HALF = S::HALF, NKS = S::NKS, NDB = S::NDB;
-  __shared__ __attribute__((aligned(16))) char kbuf[2][2 * HALF];   // [buffer][stream half]
-  __shared__ __attribute__((aligned(16))) char vbuf[2][2 * HALF];
+  // K and V buffers A and B (alternate chunks; stream s at byte HALF s).
+  // Separate variables, each named statically by every access, so that the
+  // compiler can tell a read of one chunk from the copy of the next in flight.
+  __shared__ __attribute__((aligned(16))) char kA[2 * HALF];
+  __shared__ __attribute__((aligned(16))) char kB[2 * HALF];
+  __shared__ __attribute__((aligned(16))) char vA[2 * HALF];
+  __shared__ __attribute__((aligned(16))) char vB[2 * HALF];
   int bh, r;
   group_of(a, bh, r);
   const int b = bh / a.heads, h = bh - b * a.heads;
@@ -323,27 +328,27 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
 
   unsigned zoff[S::NIW];
   swizzle_offsets<D>(qh, lane, zoff);
-  auto issue = [&](int c, int buf) {
+  auto issue = [&](int c, char* kd, char* vd) {
     const int src = src_of(c);
     unsigned offs[S::NIW];
     copy_offsets<D>(a.f, src == -1000000 ? 0 : src, sk, qh, 2u * (unsigned)st, zoff, lane, offs);
-    copy_half<D>(rk, offs, qh, kbuf[buf] + HALF * sk);
-    copy_half<D>(rv, offs, qh, vbuf[buf] + HALF * sk);
+    copy_half<D>(rk, offs, qh, kd + HALF * sk);
+    copy_half<D>(rv, offs, qh, vd + HALF * sk);
   };
 
   floatx16 acc[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db) acc[db] = floatx16{};
 
-  if (n > 0) issue(0, 0);
+  if (n > 0) issue(0, kA, vA);
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   __syncthreads();
   if (!text_group && threadIdx.x == 0) a.kmask[(int64_t)bh * a.n_tiles + (r - a.n_text_groups)] = kept_mask;
-  for (int c = 0; c < n; ++c) {
-    const int buf = c & 1;
-    if (c + 1 < n) issue(c + 1, buf ^ 1);
-    const char* kt = kbuf[buf] + HALF * sk;
-    const char* vt = vbuf[buf] + HALF * sk;
+  // Chunk c from (kc, vc) while chunk c + 1 is copied into (kn, vn).
+  auto body = [&](int c, const char* kc, const char* vc, char* kn, char* vn) {
+    if (c + 1 < n) issue(c + 1, kn, vn);
+    const char* kt = kc + HALF * sk;
+    const char* vt = vc + HALF * sk;
     // Valid keys of this stream's half: text chunks end at n_text.
     const int src = src_of(c);
     int lo = 0, hi = 32;
@@ -387,11 +392,16 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(kWaitVm0);
     __syncthreads();
+  };
+  for (int c = 0; c < n; c += 2) {
+    body(c, kA, vA, kB, vB);
+    if (c + 1 < n) body(c + 1, kB, vB, kA, vA);
   }
 
-  // Merge the two key streams through LDS (the K buffers are free now).
-  float* xo = reinterpret_cast<float*>(kbuf[0]) + (size_t)qh * 16 * NDB * 64;
-  static_assert(2 * 16 * NDB * 64 * 4 <= 2 * 2 * HALF, "merge area fits the K buffers");
+  // Merge the two key streams through LDS (the K buffers are free now):
+  // query half qh uses buffer A or B.
+  float* xo = reinterpret_cast<float*>(qh ? kB : kA);
+  static_assert(16 * NDB * 64 * 4 <= 2 * HALF, "merge area fits one K buffer");
   if (sk == 1) {
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
@@ -422,10 +432,16 @@ template <int D>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 64 ? 2 : 1))) k_bwd_dkdv(BwdArgs a) {
   using S = BShape<D>;
   constexpr int HALF = S::HALF, NKS = S::NKS, NDB = S::NDB;
-  __shared__ __attribute__((aligned(16))) char qbuf[2][2 * HALF];   // [buffer][query half]
-  __shared__ __attribute__((aligned(16))) char gbuf[2][2 * HALF];   // dO
-  __shared__ __attribute__((aligned(16))) float lbuf[2][64];         // lse2 of the chunk's rows
-  __shared__ __attribute__((aligned(16))) float dbuf[2][64];         // D of the chunk's rows
+  // Q, dO, lse2 and D buffers A and B (alternate chunks; query stream s of
+  // Q / dO at byte HALF s), separate variables as in k_bwd_dq.
+  __shared__ __attribute__((aligned(16))) char qA[2 * HALF];
+  __shared__ __attribute__((aligned(16))) char qB[2 * HALF];
+  __shared__ __attribute__((aligned(16))) char gA[2 * HALF];
+  __shared__ __attribute__((aligned(16))) char gB[2 * HALF];
+  __shared__ __attribute__((aligned(16))) float lA[64];   // lse2 of the chunk's rows
+  __shared__ __attribute__((aligned(16))) float lB[64];
+  __shared__ __attribute__((aligned(16))) float dA[64];   // D of the chunk's rows
+  __shared__ __attribute__((aligned(16))) float dB[64];
   int bh, r;
   group_of(a, bh, r);
   const int b = bh / a.heads, h = bh - b * a.heads;
@@ -502,13 +518,13 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
 
   unsigned zoff[S::NIW];
   swizzle_offsets<D>(kh, lane, zoff);
-  auto issue = [&](int src, int buf) {
+  auto issue = [&](int src, char* qd, char* gd, float* ld, float* dd) {
     unsigned offs[S::NIW];
     copy_offsets<D>(a.f, src, qs, kh, 2u * (unsigned)st, zoff, lane, offs);
-    copy_half<D>(rq, offs, kh, qbuf[buf] + HALF * qs);
-    copy_half<D>(rg, offs, kh, gbuf[buf] + HALF * qs);
-    if (w == 0) copy_rowvals(rl, a.f, src, lbuf[buf], lane);
-    if (w == 1) copy_rowvals(rdl, a.f, src, dbuf[buf], lane);
+    copy_half<D>(rq, offs, kh, qd + HALF * qs);
+    copy_half<D>(rg, offs, kh, gd + HALF * qs);
+    if (w == 0) copy_rowvals(rl, a.f, src, ld, lane);
+    if (w == 1) copy_rowvals(rdl, a.f, src, dd, lane);
   };
 
   floatx16 dk[NDB], dv[NDB];
@@ -519,15 +535,17 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
   }
 
   int src = n > 0 ? pop_src() : 0;
-  if (n > 0) issue(src, 0);
+  if (n > 0) issue(src, qA, gA, lA, dA);
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   __syncthreads();
-  for (int c = 0; c < n; ++c) {
-    const int buf = c & 1;
+  // Chunk c from the buffers (qc, gc, lc, dc) while chunk c + 1 is copied
+  // into the others.
+  auto body = [&](int c, const char* qc, const char* gc, const float* lc, const float* dc,
+                  char* qn, char* gn, float* ln, float* dn) {
     const int nsrc = c + 1 < n ? pop_src() : 0;
-    if (c + 1 < n) issue(nsrc, buf ^ 1);
-    const char* qt = qbuf[buf] + HALF * qs;
-    const char* gt = gbuf[buf] + HALF * qs;
+    if (c + 1 < n) issue(nsrc, qn, gn, ln, dn);
+    const char* qt = qc + HALF * qs;
+    const char* gt = gc + HALF * qs;
     // Valid queries of this stream's half (text chunks end at n_text).
     int hi = 32;
     if (src < 0) hi = min(max(a.f.n_text - (64 * (-1 - src) + 32 * qs), 0), 32);
@@ -535,8 +553,8 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
     float nl[16], dl[16];
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const float4 x = *reinterpret_cast<const float4*>(&lbuf[buf][32 * qs + 8 * g + 4 * hw]);
-      const float4 y = *reinterpret_cast<const float4*>(&dbuf[buf][32 * qs + 8 * g + 4 * hw]);
+      const float4 x = *reinterpret_cast<const float4*>(&lc[32 * qs + 8 * g + 4 * hw]);
+      const float4 y = *reinterpret_cast<const float4*>(&dc[32 * qs + 8 * g + 4 * hw]);
       nl[4 * g] = -x.x; nl[4 * g + 1] = -x.y; nl[4 * g + 2] = -x.z; nl[4 * g + 3] = -x.w;
       dl[4 * g] = y.x; dl[4 * g + 1] = y.y; dl[4 * g + 2] = y.z; dl[4 * g + 3] = y.w;
     }
@@ -581,12 +599,17 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
     __builtin_amdgcn_s_waitcnt(kWaitVm0);
     __syncthreads();
     src = nsrc;
+  };
+  for (int c = 0; c < n; c += 2) {
+    body(c, qA, gA, lA, dA, qB, gB, lB, dB);
+    if (c + 1 < n) body(c + 1, qB, gB, lB, dB, qA, gA, lA, dA);
   }
 
-  // Merge the two query streams through LDS (the Q / dO buffers are free).
-  static_assert(2 * 16 * NDB * 64 * 4 <= 2 * 2 * HALF, "merge area fits one buffer pair");
-  float* xk = reinterpret_cast<float*>(qbuf[0]) + (size_t)kh * 16 * NDB * 64;
-  float* xv = reinterpret_cast<float*>(gbuf[0]) + (size_t)kh * 16 * NDB * 64;
+  // Merge the two query streams through LDS (the Q / dO buffers are free):
+  // key half kh uses buffers A or B.
+  static_assert(16 * NDB * 64 * 4 <= 2 * HALF, "merge area fits one buffer");
+  float* xk = reinterpret_cast<float*>(kh ? qB : qA);
+  float* xv = reinterpret_cast<float*>(kh ? gB : gA);
   if (qs == 1) {
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
