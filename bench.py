@@ -533,7 +533,7 @@ def measure_backward(w, steps: int, warmup: int) -> dict:
         "ms_train_step": round(ms_fwd + ms_bwd, 5),
         "tflops_train_step": round((f_fwd + f_bwd) / ((ms_fwd + ms_bwd) * 1e-3) / 1e12, 2),
         "gflop_backward": round(f_bwd / 1e9, 3),
-        "roofline": {"bound": "mfma", "kernel": "k_bwd_dq + k_bwd_dkdv (+ pre-pass, transpose)",
+        "roofline": {"bound": "mfma", "kernel": "k_bwd_dq + k_bwd_dkdv",
                      "achieved": round(tf_bwd, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(tf_bwd / PEAK_BF16_TFLOPS, 4)},
     }
