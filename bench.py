@@ -305,6 +305,26 @@ def measure(w, steps: int, warmup: int, dense_steps: int, graph: bool = True):
     }
 
 
+def measured_mfma_tflops(blocks: int = 1024, iters: int = 2000, reps: int = 3) -> float:
+    """bf16 MFMA throughput the chip sustains in this process: the library's
+    probe (back-to-back v_mfma_f32_32x32x16_bf16, four waves per SIMD), best
+    of `reps` launches timed with HIP events on the stream it runs on."""
+    import torch
+    from paper_2605_15684_amd import _lib
+    sink = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    _lib.check(_lib.probe_mfma(blocks, 10, sink.data_ptr(), stream), "ssba_probe_mfma")
+    best = float("inf")
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        _lib.check(_lib.probe_mfma(blocks, iters, sink.data_ptr(), stream), "ssba_probe_mfma")
+        e1.record()
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1))
+    return blocks * 4 * iters * 8 * 32768 / (best * 1e-3) / 1e12
+
+
 def measure_layers(w, steps: int, warmup: int) -> dict:
     """A 24-layer stack through ssba_forward_layers: the synthetic per-layer
     keep schedule, the offset alternating by layer parity, every layer with
@@ -592,6 +612,7 @@ def main():
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                 "traffic": None if traffic is None else round(traffic),
                 "traffic_unit": "HBM bytes/launch", "sources_sha": sources_sha(kernel)}
+    mfma_meas = measured_mfma_tflops()
     cpu = None if args.no_cpu else cpu_baseline(r)
     line = {
         "metric": "SSBA fwd ms/call + effective TFLOP/s (% bf16 MFMA peak) at 4096 tokens, 84% sparse",
@@ -608,6 +629,8 @@ def main():
         "ms_step_cold": round(m["ms_step_cold"], 5), "ms_fwd_cold": round(m["ms_fwd_cold"], 5),
         "ms_step_graph": None if m["ms_step_graph"] is None else round(m["ms_step_graph"], 5),
         "tflops_fwd": round(m["tflops_fwd"], 2), "pct_peak_fwd": round(100 * m["tflops_fwd"] / PEAK_BF16_TFLOPS, 2),
+        "mfma_measured_tflops": round(mfma_meas, 1),
+        "pct_measured_peak_fwd": round(100 * m["tflops_fwd"] / mfma_meas, 2),
         "tflops_dense": round(m["tflops_dense"], 2),
         "speedup_vs_dense_kernel": round(m["speedup_kernel"], 3),
         "speedup_vs_dense_step": round(m["speedup_step"], 3),

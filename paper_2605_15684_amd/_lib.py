@@ -30,7 +30,8 @@ EXPORTS = ("ssba_abi_version", "ssba_status_str", "ssba_workspace_size", "ssba_b
            "ssba_forward", "ssba_forward_dense", "ssba_read_device_status",
            "ssba_forward_kernel", "ssba_forward_topk", "ssba_layers_workspace_size",
            "ssba_forward_layers", "ssba_haar_dwt", "ssba_haar_iwt", "ssba_haar_kernel_name",
-           "ssba_forward_train", "ssba_backward_workspace_size", "ssba_backward")
+           "ssba_forward_train", "ssba_backward_workspace_size", "ssba_backward",
+           "ssba_probe_mfma")
 
 
 class SsbaDesc(ctypes.Structure):
@@ -119,6 +120,8 @@ def load(path: str = None) -> ctypes.CDLL:
     lib.ssba_haar_kernel_name.argtypes = [hp, ctypes.c_int]
     lib.ssba_read_device_status.restype = ctypes.c_int
     lib.ssba_read_device_status.argtypes = [dp, vp, ctypes.POINTER(ctypes.c_int), vp]
+    lib.ssba_probe_mfma.restype = ctypes.c_int
+    lib.ssba_probe_mfma.argtypes = [ctypes.c_int32, ctypes.c_int32, vp, vp]
     _lib = lib
     return lib
 
@@ -198,6 +201,10 @@ def haar_iwt(desc, level_ptrs, residual_ptrs, x_ptr, stream) -> int:
 def haar_kernel_name(desc, inverse: bool):
     name = load().ssba_haar_kernel_name(ctypes.byref(desc), 1 if inverse else 0)
     return None if name is None else name.decode()
+
+
+def probe_mfma(blocks: int, iters: int, sink_ptr, stream) -> int:
+    return load().ssba_probe_mfma(blocks, iters, sink_ptr, stream)
 
 
 def forward_train(desc, q_ptr, k_ptr, v_ptr, index_ptr, o_ptr, lse_ptr, stream) -> int:

@@ -29,6 +29,7 @@ SOURCES = {
     "ssba_attn_mfma.hip": ["-ffp-contract=off", "-mllvm", "-amdgpu-mfma-vgpr-form"],
     "ssba_haar.hip": ["-ffp-contract=off"],
     "ssba_bwd.hip": [],
+    "ssba_probe.hip": [],
 }
 
 COMMON = [

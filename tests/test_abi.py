@@ -269,3 +269,11 @@ def test_backward_workspace_size(lib):
     rows = 2 * 3 * (10 + 4096)
     up = lambda x: (x + 255) // 256 * 256
     assert _lib.backward_workspace_size(d) == 2 * up(4 * rows) + up(8 * 2 * 3 * 64)
+
+
+def test_probe_rejects_bad_arguments(lib):
+    sink = ctypes.c_void_p(16)   # never dereferenced: every call below fails its checks first
+    assert _lib.probe_mfma(0, 10, sink, None) == _lib.SSBA_ERR_ARG
+    assert _lib.probe_mfma(4, 0, sink, None) == _lib.SSBA_ERR_ARG
+    assert _lib.probe_mfma(4, (1 << 20) + 1, sink, None) == _lib.SSBA_ERR_ARG
+    assert _lib.probe_mfma(4, 10, None, None) == _lib.SSBA_ERR_ARG
