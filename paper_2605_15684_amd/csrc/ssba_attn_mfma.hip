@@ -542,6 +542,18 @@ k_attn_mfma(AttnArgs a) {
 
   // Chunk c from buffers (kt, vt) while chunk c + 1 is copied into (kn, vn).
   auto body = [&](int c, const char* kt, const char* vt, char* kn, char* vn) {
+    // With the whole grid resident (a.equalize), the four workgroups sharing
+    // a CU would otherwise run oldest first: the youngest waits and finishes
+    // last with the SIMDs to itself.  Waves with more chunks left get the
+    // higher issue priority instead, so they finish together.  With more
+    // groups than slots the oldest-first order frees slots sooner and stays.
+    if (a.equalize) {
+      const int rem = n - c;
+      if (rem >= 24) __builtin_amdgcn_s_setprio(3);
+      else if (rem >= 8) __builtin_amdgcn_s_setprio(2);
+      else if (rem >= 4) __builtin_amdgcn_s_setprio(1);
+      else __builtin_amdgcn_s_setprio(0);
+    }
     const int lo = lo_c, hi = hi_c;
     if (c + 1 < n) {
       const Chunk cn = chunk_of(c + 1);
@@ -643,6 +655,15 @@ hipError_t launch_attn_mfma(const AttnArgs& a0, int head_dim, int tile, hipStrea
   }
   const int64_t total = (int64_t)a.batch * a.heads * a.groups_per_bh;
   if (total <= 0) return hipSuccess;
+  // Resident workgroups per CU: four waves each, four (D 64) or two (D 128)
+  // waves per SIMD.
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+    (void)hipGetLastError();   // a failed query only leaves the priorities off
+    cus = 0;
+  }
+  a.equalize = cus > 0 && total <= (int64_t)(head_dim == 64 ? 4 : 2) * cus ? 1 : 0;
   const dim3 grid((unsigned)total), block(256);
   const bool big = !a.dense && tile == 16;
   if (a.gated && (a.dense || big)) return hipErrorInvalidValue;   // gated: 8x8 blocks only

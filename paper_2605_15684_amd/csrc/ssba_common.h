@@ -95,6 +95,10 @@ struct AttnArgs {
   // Optional (MFMA kernels): natural-log log-sum-exp of each row's scaled
   // scores, [B][H][T] fp32, for the backward pass.
   float* lse;
+  // MFMA kernels, set by their launcher: 1 when every workgroup of the grid
+  // is resident at once, so the waves are prioritised by the chunks they
+  // have left (see k_attn_mfma).
+  int equalize;
 };
 
 struct IndexArgs {
