@@ -13,7 +13,11 @@ same call as ssba_build_index + ssba_forward is timed too
 stream the library launches on, once launched eagerly and once replayed from
 a HIP graph captured from the same calls (same kernels, same work; the replay
 is checked bit-exact against the eager output); `value` uses the faster.
-Index, forward and dense launches are also timed separately, back to back.
+Index, forward and dense launches, and the two-call form, are also timed
+separately, back to back: five rounds that time each form in turn, median
+per form.  The default warm-up (1000 steps) is long enough for the clock to
+settle under load: shorter ones leave the first timed milliseconds 10-15 %
+slow.
 These are warm numbers (Q, K, V and O stay in the 256 MB MALL between
 calls); ms_step_cold and ms_fwd_cold are the median of ten single calls each
 made after a 1 GiB buffer is written, so the inputs come from HBM.  Prints
@@ -57,6 +61,7 @@ import json
 import os
 import platform
 import sys
+import statistics
 import time
 
 import numpy as np
@@ -68,6 +73,7 @@ if ROOT not in sys.path:
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 COPY_BYTES = 256 << 20
+REPEATS = 5                 # rounds of the companion timings (median)
 
 # HBM traffic per launch from counter runs, keyed by kernel and workload:
 # the sources the kernel was built from (sha256 over their bytes, in order),
@@ -275,12 +281,19 @@ def measure(w, steps: int, warmup: int, dense_steps: int, graph: bool = True):
     for _ in range(warmup):
         r.step()
     wall_ms, step_ms = r.timed_steps(steps)
-    two_ms = r._span(r.step_two_calls, steps)
-    idx_ms = r._span(r.run_index, steps)
-    fwd_ms = r._span(r.run_fwd, steps)
+    # The companion timings: five rounds, each timing every call form once in
+    # turn, and the median per form, so that no form is favoured by its place
+    # in the sequence (the clock settles over the first milliseconds of load).
     for _ in range(3):
         r.run_dense()
-    dense_ms = r._span(r.run_dense, dense_steps)
+    spans = {"two": [], "idx": [], "fwd": [], "dense": []}
+    for _ in range(REPEATS):
+        spans["two"].append(r._span(r.step_two_calls, steps))
+        spans["idx"].append(r._span(r.run_index, steps))
+        spans["fwd"].append(r._span(r.run_fwd, steps))
+        spans["dense"].append(r._span(r.run_dense, dense_steps))
+    two_ms, idx_ms, fwd_ms, dense_ms = (statistics.median(spans[key])
+                                        for key in ("two", "idx", "fwd", "dense"))
     cold_step_ms = r.cold_ms(r.step)
     cold_fwd_ms = r.cold_ms(r.run_fwd)
     graph_ms = None
@@ -563,7 +576,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=1000)
     ap.add_argument("--workload", default="grid64")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--sweep", action="store_true")
@@ -576,8 +589,8 @@ def main():
                     help="measure the training forward and the backward of one SSBA call")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU: the SSBA path has no multi-GPU mode in this build "
-              "(heads and batch shard with no exchange; see the design notes).", file=sys.stderr)
+        print("bench.py measures one GPU: the SSBA path runs on one GPU here "
+              "(heads and batch would shard with no exchange).", file=sys.stderr)
         sys.exit(2)
 
     import torch
