@@ -659,7 +659,7 @@ def main():
         for c in cases:
             del r
             torch.cuda.empty_cache()
-            r, mm = measure(c, max(20, args.steps // 2), 5, 20, graph=False)
+            r, mm = measure(c, max(20, args.steps // 2), args.warmup, 20, graph=False)
             print(json.dumps({"workload": c.name, "desc": describe(c),
                               **{k: (None if v is None else round(v, 5)) for k, v in mm.items()},
                               "pct_peak_fwd": round(100 * mm["tflops_fwd"] / PEAK_BF16_TFLOPS, 2)}),
