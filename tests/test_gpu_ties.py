@@ -11,7 +11,7 @@ import pytest
 import torch
 
 from oracle import ssba_oracle as O
-from paper_2605_15684_amd.inputs import make_qkv, preset
+from paper_2605_15684_amd.inputs import make_qkv, preset, workload_from
 
 from _parity import gpu_desc, oracle_index, to64
 
@@ -42,6 +42,11 @@ CASES = [
     (preset("grid64", heads=2), 32, 63),
     (preset("grid64_text", batch=1, heads=2), 32, 10),
     (preset("grid64", heads=2, gate="topk_shared"), 32, 10),
+    # head_dim 128 (the gate's channel loop runs 128 products), 32 blocks
+    (workload_from(name="ties128", batch=1, heads=2, grid_h=32, grid_w=64, head_dim=128, tile=8,
+                   gate="topk", keep=5, shift=(4, -4), seed=13), 16, 5),
+    (workload_from(name="ties128", batch=1, heads=2, grid_h=32, grid_w=64, head_dim=128, tile=8,
+                   gate="topk", keep=5, shift=(4, -4), seed=13), 1, 5),
 ]
 
 
