@@ -237,7 +237,7 @@ __device__ __forceinline__ int gate_block(const AttnArgs& a, int bh, int i, int 
 // GATED: each image group computes its block's top-k gate first (from the
 // pooled key sums) and writes the block's index row and status flag.
 template <int D, int TILE_LOG2, bool DENSE, bool GATED>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 64 ? 4 : 2)))
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 64 ? 4 : GATED ? 2 : 3)))
 k_attn_mfma(AttnArgs a) {
   using S = Shape<D, TILE_LOG2>;
   constexpr int BT = S::BT, CPR = S::CPR, KPI = S::KPI, NIW = S::NIW, HALF = S::HALF;
@@ -249,8 +249,13 @@ k_attn_mfma(AttnArgs a) {
   // one chunk does not overlap the copy of the next still in flight.
   __shared__ __attribute__((aligned(16))) char kA[2 * HALF];
   __shared__ __attribute__((aligned(16))) char kB[2 * HALF];
+  // D 128 without the gate keeps one V buffer (48 KiB in all, three
+  // workgroups per CU): chunk c + 1's V is copied once every wave is past
+  // chunk c's products, under chunk c + 1's scores and softmax.  The gated
+  // kernel needs all four buffers for the pooled key sums.
+  constexpr bool kSingleV = D == 128 && !GATED;
   __shared__ __attribute__((aligned(16))) char vA[2 * HALF];
-  __shared__ __attribute__((aligned(16))) char vB[2 * HALF];
+  __shared__ __attribute__((aligned(16))) char vB[kSingleV ? 16 : 2 * HALF];
 
   // Logical group id.  Consecutive hardware ids go round-robin over the 8
   // XCDs; when the (batch, head) count divides by 8 each XCD gets whole
@@ -452,19 +457,25 @@ k_attn_mfma(AttnArgs a) {
   // score products start from negm = -m_run (0 while unset), so the common
   // chunk feeds the accumulator straight into exp2.
   float m_run = -1e30f, l_run = 0.f;
-  floatx16 negm = floatx16{};
+  floatx16 negm = floatx16{};   // D 64: the seed of the score products
+  float nm = 0.f;               // D 128: -m_run, added after the products (16 fewer VGPRs)
   scale_q<NKS>(qf, a.scale_log2);
   const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
 
   // One half chunk: K in kt, V in vt (this stream's halves), keys outside
   // [lo, hi) masked.
-  auto step = [&](const char* kt, const char* vt, int lo, int hi) {
+  uint32_t pk[8];   // P of the current chunk, bf16 pairs
+  auto scores = [&](const char* kt, int lo, int hi) {
     // S^T = K . Q^T: the lane's 16 keys 8 (r / 4) + 4 hw + r % 4 of its query.
-    floatx16 sc = negm;   // sc = s - m_run: the exponent of exp2 for this chunk
+    floatx16 sc = D == 64 ? negm : floatx16{};   // sc = s - m_run: the exponent of exp2
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
       const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kt + koff[ks]);
       sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sc, 0, 0, 0);
+    }
+    if constexpr (D != 64) {
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) sc[rr] += nm;
     }
     if (lo > 0 || hi < KH) {   // rare: ragged chunk or invalid block id
       int l4 = lo - 4 * hw, h4 = hi - 4 * hw;
@@ -477,7 +488,6 @@ k_attn_mfma(AttnArgs a) {
     }
     // P = exp2(sc - shift) as bf16 pairs and the lane's sum of the rounded P
     // (shift is 0 except when a chunk is redone).
-    uint32_t pk[8];
     float ls;
     auto probs = [&](float shift, bool shifted) {
       float ls0 = 0.f, ls1 = 0.f;
@@ -509,10 +519,16 @@ k_attn_mfma(AttnArgs a) {
       }
       const float mnew = m_run > -1e29f ? m_run : 0.f;
       probs(mnew - mb, true);
+      if constexpr (D == 64) {
 #pragma unroll
-      for (int rr = 0; rr < 16; ++rr) negm[rr] = -mnew;
+        for (int rr = 0; rr < 16; ++rr) negm[rr] = -mnew;
+      } else {
+        nm = -mnew;
+      }
     }
     l_run += ls;
+  };
+  auto values = [&](const char* vt) {
     // O^T[db] += V^T . P^T over 2 key steps of 16 (V^T operands: keys
     // 16 ks + 8 (e / 4) + 4 hw + e % 4, channel 32 db + lane % 32).
 #pragma unroll
@@ -540,13 +556,12 @@ k_attn_mfma(AttnArgs a) {
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   __syncthreads();
 
-  // Chunk c from buffers (kt, vt) while chunk c + 1 is copied into (kn, vn).
-  auto body = [&](int c, const char* kt, const char* vt, char* kn, char* vn) {
-    // With the whole grid resident (a.equalize), the four workgroups sharing
-    // a CU would otherwise run oldest first: the youngest waits and finishes
-    // last with the SIMDs to itself.  Waves with more chunks left get the
-    // higher issue priority instead, so they finish together.  With more
-    // groups than slots the oldest-first order frees slots sooner and stays.
+  // With the whole grid resident (a.equalize), the workgroups sharing a CU
+  // would otherwise run oldest first: the youngest waits and finishes last
+  // with the SIMDs to itself.  Waves with more chunks left get the higher
+  // issue priority instead, so they finish together.  With more groups than
+  // slots the oldest-first order frees slots sooner and stays.
+  auto prioritise = [&](int c) {
     if (a.equalize) {
       const int rem = n - c;
       if (rem >= 24) __builtin_amdgcn_s_setprio(3);
@@ -554,6 +569,10 @@ k_attn_mfma(AttnArgs a) {
       else if (rem >= 4) __builtin_amdgcn_s_setprio(1);
       else __builtin_amdgcn_s_setprio(0);
     }
+  };
+  // Chunk c from buffers (kt, vt) while chunk c + 1 is copied into (kn, vn).
+  auto body = [&](int c, const char* kt, const char* vt, char* kn, char* vn) {
+    prioritise(c);
     const int lo = lo_c, hi = hi_c;
     if (c + 1 < n) {
       const Chunk cn = chunk_of(c + 1);
@@ -562,7 +581,8 @@ k_attn_mfma(AttnArgs a) {
       lo_c = cn.lo;
       hi_c = cn.hi;
     }
-    step(kt, vt, lo, hi);
+    scores(kt, lo, hi);
+    values(vt);
     // The products are issued before the wait, so they run during it.
     __builtin_amdgcn_sched_barrier(0);
     // Chunk c + 1 has landed (this wave's part) and every wave is past its
@@ -570,9 +590,48 @@ k_attn_mfma(AttnArgs a) {
     __builtin_amdgcn_s_waitcnt(kWaitVm0);
     __syncthreads();
   };
-  for (int c = 0; c < n; c += 2) {
-    body(c, kA, vA, kB, vB);
-    if (c + 1 < n) body(c + 1, kB, vB, kA, vA);
+  // One V buffer: chunk c from (kt, vA) while chunk c + 1's K is copied into
+  // kn; chunk c + 1's V follows once every wave is past chunk c's products.
+  auto body_single_v = [&](int c, const char* kt, char* kn) {
+    prioritise(c);
+    const int lo = lo_c, hi = hi_c;
+    const bool more = c + 1 < n;
+    Chunk cn;
+    if (more) {
+      cn = chunk_of(c + 1);
+      lo_c = cn.lo;
+      hi_c = cn.hi;
+    } else {
+      // No next chunk: the same number of copies, every one past the end of
+      // the buffer range (no memory traffic; zeros land in kn, unread), so
+      // the wait below counts the same on every path.
+      cn.row0 = 0;
+      cn.rstep = 0;
+      cn.y0 = 0;
+#pragma unroll
+      for (int mm = 0; mm < NIW; ++mm) cn.lane_off[mm] = 0x80000000u;
+    }
+    copy(rk, cn, kn, true);
+    scores(kt, lo, hi);
+    // Chunk c's V (copied before chunk c + 1's K) has landed in every wave.
+    __builtin_amdgcn_s_waitcnt(kWaitVm0 | NIW);
+    __syncthreads();
+    values(vA);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(kWaitVm0);
+    __syncthreads();
+    if (more) copy(rv, cn, vA, false);
+  };
+  if constexpr (kSingleV) {
+    for (int c = 0; c < n; c += 2) {
+      body_single_v(c, kA, kB);
+      if (c + 1 < n) body_single_v(c + 1, kB, kA);
+    }
+  } else {
+    for (int c = 0; c < n; c += 2) {
+      body(c, kA, vA, kB, vB);
+      if (c + 1 < n) body(c + 1, kB, vB, kA, vA);
+    }
   }
 
   // Merge the two key streams: stream 1 leaves (m, l, O) in LDS, stream 0
@@ -655,15 +714,16 @@ hipError_t launch_attn_mfma(const AttnArgs& a0, int head_dim, int tile, hipStrea
   }
   const int64_t total = (int64_t)a.batch * a.heads * a.groups_per_bh;
   if (total <= 0) return hipSuccess;
-  // Resident workgroups per CU: four waves each, four (D 64) or two (D 128)
-  // waves per SIMD.
+  // Resident workgroups per CU: four waves each, four (D 64), three (D 128
+  // with one V buffer) or two (gated D 128) waves per SIMD.
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
     (void)hipGetLastError();   // a failed query only leaves the priorities off
     cus = 0;
   }
-  a.equalize = cus > 0 && total <= (int64_t)(head_dim == 64 ? 4 : 2) * cus ? 1 : 0;
+  const int slots = head_dim == 64 ? 4 : (a.gated && !a.dense) ? 2 : 3;
+  a.equalize = cus > 0 && total <= (int64_t)slots * cus ? 1 : 0;
   const dim3 grid((unsigned)total), block(256);
   const bool big = !a.dense && tile == 16;
   if (a.gated && (a.dense || big)) return hipErrorInvalidValue;   // gated: 8x8 blocks only
