@@ -84,7 +84,7 @@ MEASURED_TRAFFIC = {
     ("k_haar_dwt<unsigned short, 3>", "haar512"): {"sha": "02be9c317bd1aa8b", "fetch_kib": 131115.0,
                                                   "write_kib": 344064.0, "fetch_factor": 1.9998,
                                                   "write_factor": 1.0},
-    ("k_attn_mfma<64, 3, false, false>", "grid64"): {"sha": "313ac85f23b3db8e", "fetch_kib": 12554.2,
+    ("k_attn_mfma<64, 3, false, false>", "grid64"): {"sha": "1e4d38cadd42d5de", "fetch_kib": 12554.1,
                                                      "write_kib": 8192.0, "fetch_factor": 1.9998,
                                                      "write_factor": 1.0},
 }
