@@ -23,8 +23,8 @@ from typing import Optional, Tuple
 
 import torch
 
-__all__ = ["Workload", "PRESETS", "preset", "make_qkv", "workload_from", "LAYER_KEEP_SCHEDULE_24",
-           "LAYER_SKIP_24"]
+__all__ = ["Workload", "PRESETS", "preset", "make_qkv", "workload_from", "heavy_key_rows",
+           "LAYER_KEEP_SCHEDULE_24", "LAYER_SKIP_24"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -124,6 +124,17 @@ def workload_from(**kw) -> Workload:
 
 
 _TORCH_DTYPES = {"bf16": torch.bfloat16, "f32": torch.float32}
+
+
+def heavy_key_rows(w: Workload) -> torch.Tensor:
+    """Image token ids (0 .. T_img - 1) of the key rows that make_qkv scales
+    by 8, sorted; empty when the workload has none.  Replays the same seeded
+    draws as make_qkv."""
+    if w.heavy_key_rows <= 0:
+        return torch.empty(0, dtype=torch.int64)
+    g = torch.Generator(device="cpu").manual_seed(int(w.seed))
+    torch.randn((3, w.batch, w.heads, w.seq_len, w.head_dim), generator=g, dtype=torch.float32)
+    return torch.sort(torch.randperm(w.t_img, generator=g)[: w.heavy_key_rows]).values
 
 
 def make_qkv(w: Workload, device: Optional[str] = None):

@@ -15,7 +15,7 @@ import torch
 
 from oracle import ssba_oracle as O
 from paper_2605_15684_amd.inputs import preset, workload_from
-from tests._parity import gpu_desc, inputs, oracle_kw, to64
+from tests._parity import gpu_desc, inputs, oracle_index, oracle_kw, to64
 
 pytestmark = pytest.mark.gpu
 
@@ -38,7 +38,11 @@ def _run(w, heads=None):
     dout = _dout(w)
     dq, dk, dv = ssba.backward(qg, kg, vg, out, dout.to("cuda"), lse, index, desc)
     torch.cuda.synchronize()
-    ref = O.attention_backward(to64(q), to64(k), to64(v), to64(dout), index.cpu().numpy(),
+    # The reference gradients use the oracle's own gate: the GPU index must
+    # equal it bit for bit first, so a wrong gate cannot pass on both sides.
+    want_idx = oracle_index(w, q, k)
+    assert np.array_equal(index.cpu().numpy(), want_idx), "GPU index differs from the oracle's"
+    ref = O.attention_backward(to64(q), to64(k), to64(v), to64(dout), want_idx,
                                heads=heads, **oracle_kw(w))
     return (dq, dk, dv, lse), ref
 

@@ -90,3 +90,37 @@ def test_levels_transform_the_unrounded_ll_and_residuals_add():
     w1[:, :, 0] = ll1 + r1
     want = H.iwt_level(w1) + r0
     np.testing.assert_allclose(got, want, atol=1e-12)
+
+
+def test_reading_of_the_band_subscript_matches_the_stated_shape():
+    """The DWT equation writes level l as the Haar bank applied to W^(l-1)_c
+    with c = {LL, HL, LH}, and gives W^(l) 4C channels at H/2^l x W/2^l for
+    every l with one C.  Reading: level l transforms the LL band of level
+    l - 1 (the Mallat pyramid); c names the bands the encoder keeps from each
+    level (all four are stored).  Pinned two ways:
+      * the pyramid written with 1-D Haar matrices -- level 2 is the
+        Kronecker transform of level 1's low/low quadrant -- equals the
+        oracle's level 2, band by band;
+      * the shapes: the oracle's level l has 4C channels for every l, while
+        transforming the three bands {LL, HL, LH} of level 1 would give 12C
+        channels at level 2, which the stated shape rules out."""
+    rng = np.random.default_rng(11)
+    c, h, w_ = 2, 16, 16
+    x = rng.standard_normal((1, c, h, w_))
+    lv = H.dwt(x, 3)
+    for l, wl in enumerate(lv, start=1):
+        assert wl.shape == (1, 4 * c, h >> l, w_ >> l)
+    for ch in range(c):
+        y1 = _haar_1d(h) @ x[0, ch] @ _haar_1d(w_).T                 # level 1, quadrant form
+        ll1 = y1[: h // 2, : w_ // 2]
+        y2 = _haar_1d(h // 2) @ ll1 @ _haar_1d(w_ // 2).T            # level 2 from LL only
+        q = h // 4
+        got = lv[1][0, 4 * ch: 4 * ch + 4]
+        np.testing.assert_allclose(got[0], y2[:q, :q], atol=1e-12)   # LL
+        np.testing.assert_allclose(got[1], y2[:q, q:], atol=1e-12)   # HL
+        np.testing.assert_allclose(got[2], y2[q:, :q], atol=1e-12)   # LH
+        np.testing.assert_allclose(got[3], y2[q:, q:], atol=1e-12)   # HH
+    # The other reading: the bank applied to the three kept bands of level 1.
+    kept = lv[0].reshape(1, c, 4, h // 2, w_ // 2)[:, :, :3].reshape(1, 3 * c, h // 2, w_ // 2)
+    other = H.dwt(kept, 1)[0]
+    assert other.shape[1] == 12 * c != 4 * c
