@@ -52,6 +52,14 @@
  * Errors: descriptor and pointer checks happen before anything is launched;
  * on a non-zero status nothing has been enqueued and outputs are untouched.
  * SSBA_ERR_HIP reports a failed launch (hipGetLastError).
+ *
+ * Buffer sizes: every entry point that takes `index` or `scratch` has an
+ * `_ex` form that also takes their sizes in bytes (`index_bytes`,
+ * `scratch_bytes`) and returns SSBA_ERR_WORKSPACE, before anything is
+ * launched, when a buffer is shorter than the call needs (the sizes that
+ * ssba_workspace_size, ssba_layers_workspace_size or
+ * ssba_backward_workspace_size report).  The forms without sizes check
+ * nothing: the caller vouches for the buffers.
  */
 #ifndef SSBA_H_
 #define SSBA_H_
@@ -63,14 +71,14 @@
 extern "C" {
 #endif
 
-#define SSBA_ABI_VERSION 2
+#define SSBA_ABI_VERSION 3
 
 typedef enum {
   SSBA_OK = 0,
   SSBA_ERR_ARG = 1,          /* null pointer, bad enum, bad keep / window   */
   SSBA_ERR_SHAPE = 2,        /* non-positive sizes, grid not a multiple of Bt */
   SSBA_ERR_UNSUPPORTED = 3,  /* head_dim / tile / block count not built     */
-  SSBA_ERR_WORKSPACE = 4,    /* (reserved)                                  */
+  SSBA_ERR_WORKSPACE = 4,    /* index / scratch buffer shorter than needed  */
   SSBA_ERR_NONFINITE = 5,    /* gate saw a NaN/Inf affinity (device status) */
   SSBA_ERR_HIP = 6           /* HIP launch or copy failure                  */
 } ssba_status;
@@ -123,6 +131,10 @@ ssba_status ssba_workspace_size(const ssba_desc* d, size_t* index_bytes, size_t*
 ssba_status ssba_build_index(const ssba_desc* d, const void* q, const void* k,
                              int32_t* index, void* scratch, void* hip_stream);
 
+/* ssba_build_index with the sizes of `index` and `scratch` in bytes. */
+ssba_status ssba_build_index_ex(const ssba_desc* d, const void* q, const void* k, int32_t* index,
+                                size_t index_bytes, void* scratch, size_t scratch_bytes, void* hip_stream);
+
 /* SSBA attention (Algorithm 1, attend step): O = softmax(scale * Q K^T + mask) V
  * where an image query in block i sees the image keys of the blocks listed in
  * index[b][h][i] and every text key; a text query sees every key.  Masked
@@ -134,6 +146,10 @@ ssba_status ssba_build_index(const ssba_desc* d, const void* q, const void* k,
  * (counts in 0..T_b, ids in 0..T_b-1; other contents are undefined behaviour). */
 ssba_status ssba_forward(const ssba_desc* d, const void* q, const void* k, const void* v,
                          const int32_t* index, void* o, void* hip_stream);
+
+/* ssba_forward with the size of `index` in bytes. */
+ssba_status ssba_forward_ex(const ssba_desc* d, const void* q, const void* k, const void* v,
+                            const int32_t* index, size_t index_bytes, void* o, void* hip_stream);
 
 /* Dense attention in the same kernel family (the zero-sparsity control of
  * Section 2.2.1's cost comparison): every query sees all T keys; the gate,
@@ -155,6 +171,11 @@ ssba_status ssba_forward_dense(const ssba_desc* d, const void* q, const void* k,
 ssba_status ssba_forward_topk(const ssba_desc* d, const void* q, const void* k, const void* v,
                               int32_t* index, void* scratch, void* o, void* hip_stream);
 
+/* ssba_forward_topk with the sizes of `index` and `scratch` in bytes. */
+ssba_status ssba_forward_topk_ex(const ssba_desc* d, const void* q, const void* k, const void* v,
+                                 int32_t* index, size_t index_bytes, void* scratch, size_t scratch_bytes,
+                                 void* o, void* hip_stream);
+
 /* Training forward: ssba_forward plus `lse`, fp32 [B][H][T], the natural-log
  * log-sum-exp of each row's scaled scores (log of the softmax normaliser,
  * log sum_j exp(scale q . k_j) over the row's visible keys), which
@@ -163,6 +184,11 @@ ssba_status ssba_forward_topk(const ssba_desc* d, const void* q, const void* k, 
  * aligned, caller-owned. */
 ssba_status ssba_forward_train(const ssba_desc* d, const void* q, const void* k, const void* v,
                                const int32_t* index, void* o, float* lse, void* hip_stream);
+
+/* ssba_forward_train with the size of `index` in bytes. */
+ssba_status ssba_forward_train_ex(const ssba_desc* d, const void* q, const void* k, const void* v,
+                                  const int32_t* index, size_t index_bytes, void* o, float* lse,
+                                  void* hip_stream);
 
 /* Device bytes of the scratch ssba_backward needs (256-byte aligned buffer):
  * fp32 [B][H][T] twice (the log-sum-exp in log2 units and rowsum(dO * O)) and
@@ -186,6 +212,12 @@ ssba_status ssba_backward_workspace_size(const ssba_desc* d, size_t* scratch_byt
 ssba_status ssba_backward(const ssba_desc* d, const void* q, const void* k, const void* v, const void* o,
                           const void* dout, const float* lse, const int32_t* index, void* dq, void* dk,
                           void* dv, void* scratch, void* hip_stream);
+
+/* ssba_backward with the sizes of `index` and `scratch` in bytes. */
+ssba_status ssba_backward_ex(const ssba_desc* d, const void* q, const void* k, const void* v, const void* o,
+                             const void* dout, const float* lse, const int32_t* index, size_t index_bytes,
+                             void* dq, void* dk, void* dv, void* scratch, size_t scratch_bytes,
+                             void* hip_stream);
 
 /* One layer of a stack run by ssba_forward_layers. */
 typedef struct ssba_layer {
@@ -221,6 +253,12 @@ ssba_status ssba_layers_workspace_size(const ssba_desc* d, int n_layers, size_t*
 ssba_status ssba_forward_layers(const ssba_desc* d, const ssba_layer* layers, int n_layers,
                                 int32_t* index, void* scratch, void* hip_stream);
 
+/* ssba_forward_layers with the sizes of `index` and `scratch` in bytes (the
+ * whole stack's, as ssba_layers_workspace_size reports them). */
+ssba_status ssba_forward_layers_ex(const ssba_desc* d, const ssba_layer* layers, int n_layers,
+                                   int32_t* index, size_t index_bytes, void* scratch, size_t scratch_bytes,
+                                   void* hip_stream);
+
 /* Name of the attention kernel that ssba_forward (mode 0), ssba_forward_dense
  * (mode 1) or ssba_forward_topk (mode 2) launches for this descriptor, as
  * profilers show it without namespace and arguments (e.g.
@@ -234,6 +272,10 @@ const char* ssba_forward_kernel(const ssba_desc* d, int mode);
  * for the shared gate, the summed row).  d->keep is not used here. */
 ssba_status ssba_read_device_status(const ssba_desc* d, const void* scratch, ssba_status* out,
                                     void* hip_stream);
+
+/* ssba_read_device_status with the size of `scratch` in bytes. */
+ssba_status ssba_read_device_status_ex(const ssba_desc* d, const void* scratch, size_t scratch_bytes,
+                                       ssba_status* out, void* hip_stream);
 
 #ifdef __cplusplus
 }

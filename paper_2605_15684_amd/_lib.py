@@ -31,7 +31,12 @@ EXPORTS = ("ssba_abi_version", "ssba_status_str", "ssba_workspace_size", "ssba_b
            "ssba_forward_kernel", "ssba_forward_topk", "ssba_layers_workspace_size",
            "ssba_forward_layers", "ssba_haar_dwt", "ssba_haar_iwt", "ssba_haar_kernel_name",
            "ssba_forward_train", "ssba_backward_workspace_size", "ssba_backward",
-           "ssba_probe_mfma")
+           "ssba_probe_mfma", "ssba_build_index_ex", "ssba_forward_ex", "ssba_forward_topk_ex",
+           "ssba_forward_train_ex", "ssba_backward_ex", "ssba_forward_layers_ex",
+           "ssba_read_device_status_ex")
+
+# Byte count that the binding passes for a buffer it cannot size (None).
+UNSIZED = ctypes.c_size_t(-1).value
 
 
 class SsbaDesc(ctypes.Structure):
@@ -122,6 +127,17 @@ def load(path: str = None) -> ctypes.CDLL:
     lib.ssba_read_device_status.argtypes = [dp, vp, ctypes.POINTER(ctypes.c_int), vp]
     lib.ssba_probe_mfma.restype = ctypes.c_int
     lib.ssba_probe_mfma.argtypes = [ctypes.c_int32, ctypes.c_int32, vp, vp]
+    for name, args in (("ssba_build_index_ex", [dp, vp, vp, vp, sz, vp, sz, vp]),
+                       ("ssba_forward_ex", [dp, vp, vp, vp, vp, sz, vp, vp]),
+                       ("ssba_forward_topk_ex", [dp, vp, vp, vp, vp, sz, vp, sz, vp, vp]),
+                       ("ssba_forward_train_ex", [dp, vp, vp, vp, vp, sz, vp, vp, vp]),
+                       ("ssba_backward_ex", [dp, vp, vp, vp, vp, vp, vp, vp, sz, vp, vp, vp, vp, sz, vp]),
+                       ("ssba_forward_layers_ex", [dp, ctypes.POINTER(SsbaLayer), ctypes.c_int, vp, sz, vp, sz,
+                                                   vp]),
+                       ("ssba_read_device_status_ex", [dp, vp, sz, ctypes.POINTER(ctypes.c_int), vp])):
+        fn = getattr(lib, name)
+        fn.restype = ctypes.c_int
+        fn.argtypes = args
     _lib = lib
     return lib
 
@@ -142,28 +158,37 @@ def workspace_size(desc: SsbaDesc):
     return ib.value, sb.value
 
 
-def build_index(desc, q_ptr, k_ptr, index_ptr, scratch_ptr, stream) -> int:
-    return load().ssba_build_index(ctypes.byref(desc), q_ptr, k_ptr, index_ptr, scratch_ptr, stream)
+def _nb(n):
+    return UNSIZED if n is None else int(n)
 
 
-def forward(desc, q_ptr, k_ptr, v_ptr, index_ptr, o_ptr, stream) -> int:
-    return load().ssba_forward(ctypes.byref(desc), q_ptr, k_ptr, v_ptr, index_ptr, o_ptr, stream)
+def build_index(desc, q_ptr, k_ptr, index_ptr, scratch_ptr, stream, index_bytes=None,
+                scratch_bytes=None) -> int:
+    """ssba_build_index_ex; a size of None is passed as unchecked."""
+    return load().ssba_build_index_ex(ctypes.byref(desc), q_ptr, k_ptr, index_ptr, _nb(index_bytes),
+                                      scratch_ptr, _nb(scratch_bytes), stream)
+
+
+def forward(desc, q_ptr, k_ptr, v_ptr, index_ptr, o_ptr, stream, index_bytes=None) -> int:
+    return load().ssba_forward_ex(ctypes.byref(desc), q_ptr, k_ptr, v_ptr, index_ptr, _nb(index_bytes),
+                                  o_ptr, stream)
 
 
 def forward_dense(desc, q_ptr, k_ptr, v_ptr, o_ptr, stream) -> int:
     return load().ssba_forward_dense(ctypes.byref(desc), q_ptr, k_ptr, v_ptr, o_ptr, stream)
 
 
-def read_device_status(desc, scratch_ptr, stream):
+def read_device_status(desc, scratch_ptr, stream, scratch_bytes=None):
     out = ctypes.c_int(0)
-    check(load().ssba_read_device_status(ctypes.byref(desc), scratch_ptr, ctypes.byref(out), stream),
-          "ssba_read_device_status")
+    check(load().ssba_read_device_status_ex(ctypes.byref(desc), scratch_ptr, _nb(scratch_bytes),
+                                            ctypes.byref(out), stream), "ssba_read_device_status")
     return out.value
 
 
-def forward_topk(desc, q_ptr, k_ptr, v_ptr, index_ptr, scratch_ptr, o_ptr, stream) -> int:
-    return load().ssba_forward_topk(ctypes.byref(desc), q_ptr, k_ptr, v_ptr, index_ptr, scratch_ptr,
-                                    o_ptr, stream)
+def forward_topk(desc, q_ptr, k_ptr, v_ptr, index_ptr, scratch_ptr, o_ptr, stream, index_bytes=None,
+                 scratch_bytes=None) -> int:
+    return load().ssba_forward_topk_ex(ctypes.byref(desc), q_ptr, k_ptr, v_ptr, index_ptr, _nb(index_bytes),
+                                       scratch_ptr, _nb(scratch_bytes), o_ptr, stream)
 
 
 def forward_kernel(desc, dense: bool = False, mode: int = None):
@@ -181,10 +206,10 @@ def layers_workspace_size(desc: SsbaDesc, n_layers: int):
     return ib.value, sb.value
 
 
-def forward_layers(desc, layers, index_ptr, scratch_ptr, stream) -> int:
+def forward_layers(desc, layers, index_ptr, scratch_ptr, stream, index_bytes=None, scratch_bytes=None) -> int:
     """`layers`: a ctypes array of SsbaLayer."""
-    return load().ssba_forward_layers(ctypes.byref(desc), layers, len(layers), index_ptr, scratch_ptr,
-                                      stream)
+    return load().ssba_forward_layers_ex(ctypes.byref(desc), layers, len(layers), index_ptr, _nb(index_bytes),
+                                         scratch_ptr, _nb(scratch_bytes), stream)
 
 
 def haar_dwt(desc, x_ptr, level_ptrs, stream) -> int:
@@ -207,8 +232,9 @@ def probe_mfma(blocks: int, iters: int, sink_ptr, stream) -> int:
     return load().ssba_probe_mfma(blocks, iters, sink_ptr, stream)
 
 
-def forward_train(desc, q_ptr, k_ptr, v_ptr, index_ptr, o_ptr, lse_ptr, stream) -> int:
-    return load().ssba_forward_train(ctypes.byref(desc), q_ptr, k_ptr, v_ptr, index_ptr, o_ptr, lse_ptr, stream)
+def forward_train(desc, q_ptr, k_ptr, v_ptr, index_ptr, o_ptr, lse_ptr, stream, index_bytes=None) -> int:
+    return load().ssba_forward_train_ex(ctypes.byref(desc), q_ptr, k_ptr, v_ptr, index_ptr, _nb(index_bytes),
+                                        o_ptr, lse_ptr, stream)
 
 
 def backward_workspace_size(desc) -> int:
@@ -217,5 +243,7 @@ def backward_workspace_size(desc) -> int:
     return sb.value
 
 
-def backward(desc, q, k, v, o, dout, lse, index, dq, dk, dv, scratch, stream) -> int:
-    return load().ssba_backward(ctypes.byref(desc), q, k, v, o, dout, lse, index, dq, dk, dv, scratch, stream)
+def backward(desc, q, k, v, o, dout, lse, index, dq, dk, dv, scratch, stream, index_bytes=None,
+             scratch_bytes=None) -> int:
+    return load().ssba_backward_ex(ctypes.byref(desc), q, k, v, o, dout, lse, index, _nb(index_bytes), dq, dk,
+                                   dv, scratch, _nb(scratch_bytes), stream)

@@ -20,6 +20,7 @@ ARCH = os.environ.get("SSBA_OFFLOAD_ARCH", "gfx950")
 
 SOURCES = {
     "ssba_api.cpp": [],
+    "ssba_select.cpp": [],
     # fp64 gate: no contraction of multiply-add, so lists are bit-reproducible.
     "ssba_index.hip": ["-ffp-contract=off"],
     "ssba_attn_bf16.hip": [],

@@ -73,6 +73,14 @@ ssba_status check_desc(const ssba_desc* d, Shape* out, bool gate_fields = true) 
   // Element offsets must stay inside int64 and row indices inside int32.
   const double span = (double)(d->batch - 1) * sb + (double)(d->heads - 1) * sh + (double)seq * st;
   if (span > 9.0e18) return SSBA_ERR_SHAPE;
+  // Workspace byte counts (index, pooled sums, per-head affinity rows) must
+  // not wrap around size_t, and a launch covers every (batch, head) pair's
+  // query groups with fewer than 2^31 workgroups.
+  const double pairs = (double)d->batch * d->heads;
+  if (pairs * (double)n_tiles * (double)(n_tiles + 1) * 8.0 > 9.0e18 ||
+      pairs * (double)n_tiles * (double)d->head_dim * 16.0 > 9.0e18)
+    return SSBA_ERR_SHAPE;
+  if (pairs * (double)(seq / 64 + 1 + n_tiles * 4) >= 2147483648.0) return SSBA_ERR_UNSUPPORTED;
   if (out) {
     out->sb = sb;
     out->sh = sh;
@@ -93,6 +101,10 @@ ssba_status check_desc(const ssba_desc* d, Shape* out, bool gate_fields = true) 
 }
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Byte count passed by the entry points without a size argument: the caller
+// vouches for the buffer, nothing is checked.
+constexpr size_t kUnchecked = SIZE_MAX;
 
 size_t index_bytes_of(const ssba_desc* d, const Shape& s) {
   return (size_t)4 * d->batch * d->heads * s.n_tiles * (s.n_tiles + 1);
@@ -160,7 +172,7 @@ AttnArgs attn_args(const ssba_desc* d, const Shape& s, const void* q, const void
 }
 
 ssba_status run_attention(const ssba_desc* d, const void* q, const void* k, const void* v,
-                          const int32_t* index, void* o, void* stream, bool dense) {
+                          const int32_t* index, size_t index_bytes, void* o, void* stream, bool dense) {
   Shape s;
   ssba_status st = check_desc(d, &s, !dense);
   if (st != SSBA_OK) return st;
@@ -168,6 +180,7 @@ ssba_status run_attention(const ssba_desc* d, const void* q, const void* k, cons
   const size_t al = d->dtype == SSBA_DT_BF16 ? 16 : 4;
   if (!aligned(q, al) || !aligned(k, al) || !aligned(v, al) || !aligned(o, al) || !aligned(index, 4))
     return SSBA_ERR_ARG;
+  if (!dense && index_bytes < index_bytes_of(d, s)) return SSBA_ERR_WORKSPACE;
   const AttnArgs a = attn_args(d, s, q, k, v, index, o, dense);
   hipStream_t hs = static_cast<hipStream_t>(stream);
   hipError_t e = d->dtype == SSBA_DT_BF16 ? ssba::launch_attn_bf16(a, d->head_dim, d->tile, hs)
@@ -247,8 +260,8 @@ bool gated_supported(const ssba_desc* d, const Shape& s) {
 
 extern "C" {
 
-ssba_status ssba_build_index(const ssba_desc* d, const void* q, const void* k, int32_t* index,
-                             void* scratch, void* stream) {
+ssba_status ssba_build_index_ex(const ssba_desc* d, const void* q, const void* k, int32_t* index,
+                                size_t index_bytes, void* scratch, size_t scratch_bytes, void* stream) {
   Shape s;
   const ssba_status st = check_desc(d, &s);
   if (st != SSBA_OK) return st;
@@ -258,6 +271,7 @@ ssba_status ssba_build_index(const ssba_desc* d, const void* q, const void* k, i
     const size_t al = d->dtype == SSBA_DT_BF16 ? 16 : 4;
     if (!q || !k || !aligned(q, al) || !aligned(k, al)) return SSBA_ERR_ARG;
   }
+  if (index_bytes < index_bytes_of(d, s) || scratch_bytes < scratch_bytes_of(d, s)) return SSBA_ERR_WORKSPACE;
   const IndexArgs a = index_args(d, s, q, k, index, scratch);
   hipStream_t hs = static_cast<hipStream_t>(stream);
   hipError_t e;
@@ -271,8 +285,29 @@ ssba_status ssba_build_index(const ssba_desc* d, const void* q, const void* k, i
   return e == hipSuccess ? SSBA_OK : SSBA_ERR_HIP;
 }
 
-ssba_status ssba_forward_topk(const ssba_desc* d, const void* q, const void* k, const void* v,
-                              int32_t* index, void* scratch, void* o, void* stream) {
+ssba_status ssba_build_index(const ssba_desc* d, const void* q, const void* k, int32_t* index,
+                             void* scratch, void* stream) {
+  return ssba_build_index_ex(d, q, k, index, kUnchecked, scratch, kUnchecked, stream);
+}
+
+ssba_status ssba_forward_ex(const ssba_desc* d, const void* q, const void* k, const void* v,
+                            const int32_t* index, size_t index_bytes, void* o, void* stream) {
+  return run_attention(d, q, k, v, index, index_bytes, o, stream, false);
+}
+
+ssba_status ssba_forward(const ssba_desc* d, const void* q, const void* k, const void* v,
+                         const int32_t* index, void* o, void* stream) {
+  return run_attention(d, q, k, v, index, kUnchecked, o, stream, false);
+}
+
+ssba_status ssba_forward_dense(const ssba_desc* d, const void* q, const void* k, const void* v,
+                               void* o, void* stream) {
+  return run_attention(d, q, k, v, nullptr, kUnchecked, o, stream, true);
+}
+
+ssba_status ssba_forward_topk_ex(const ssba_desc* d, const void* q, const void* k, const void* v,
+                                 int32_t* index, size_t index_bytes, void* scratch, size_t scratch_bytes,
+                                 void* o, void* stream) {
   Shape s;
   ssba_status st = check_desc(d, &s);
   if (st != SSBA_OK) return st;
@@ -282,9 +317,10 @@ ssba_status ssba_forward_topk(const ssba_desc* d, const void* q, const void* k, 
   if (!aligned(q, al) || !aligned(k, al) || !aligned(v, al) || !aligned(o, al) || !aligned(index, 4) ||
       !aligned(scratch, 16))
     return SSBA_ERR_ARG;
+  if (index_bytes < index_bytes_of(d, s) || scratch_bytes < scratch_bytes_of(d, s)) return SSBA_ERR_WORKSPACE;
   if (d->gate != SSBA_GATE_TOPK || !gated_supported(d, s)) {   // the two calls, same results
-    st = ssba_build_index(d, q, k, index, scratch, stream);
-    return st != SSBA_OK ? st : ssba_forward(d, q, k, v, index, o, stream);
+    st = ssba_build_index_ex(d, q, k, index, index_bytes, scratch, scratch_bytes, stream);
+    return st != SSBA_OK ? st : ssba_forward_ex(d, q, k, v, index, index_bytes, o, stream);
   }
   IndexArgs ia = index_args(d, s, q, k, index, scratch);
   AttnArgs aa = attn_args(d, s, q, k, v, nullptr, o, false);
@@ -300,6 +336,11 @@ ssba_status ssba_forward_topk(const ssba_desc* d, const void* q, const void* k, 
   return e == hipSuccess ? SSBA_OK : SSBA_ERR_HIP;
 }
 
+ssba_status ssba_forward_topk(const ssba_desc* d, const void* q, const void* k, const void* v,
+                              int32_t* index, void* scratch, void* o, void* stream) {
+  return ssba_forward_topk_ex(d, q, k, v, index, kUnchecked, scratch, kUnchecked, o, stream);
+}
+
 const char* ssba_forward_kernel(const ssba_desc* d, int mode) {
   Shape s;
   const bool dense = mode == 1;
@@ -310,18 +351,9 @@ const char* ssba_forward_kernel(const ssba_desc* d, int mode) {
   return ssba::attn_kernel_name(a, d->head_dim, d->tile, d->dtype);
 }
 
-ssba_status ssba_forward(const ssba_desc* d, const void* q, const void* k, const void* v,
-                         const int32_t* index, void* o, void* stream) {
-  return run_attention(d, q, k, v, index, o, stream, false);
-}
-
-ssba_status ssba_forward_dense(const ssba_desc* d, const void* q, const void* k, const void* v,
-                               void* o, void* stream) {
-  return run_attention(d, q, k, v, nullptr, o, stream, true);
-}
-
-ssba_status ssba_forward_train(const ssba_desc* d, const void* q, const void* k, const void* v,
-                               const int32_t* index, void* o, float* lse, void* stream) {
+ssba_status ssba_forward_train_ex(const ssba_desc* d, const void* q, const void* k, const void* v,
+                                  const int32_t* index, size_t index_bytes, void* o, float* lse,
+                                  void* stream) {
   Shape s;
   const ssba_status st = check_desc(d, &s, false);
   if (st != SSBA_OK) return st;
@@ -332,10 +364,16 @@ ssba_status ssba_forward_train(const ssba_desc* d, const void* q, const void* k,
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16) || !aligned(index, 4) ||
       !aligned(lse, 4))
     return SSBA_ERR_ARG;
+  if (index_bytes < index_bytes_of(d, s)) return SSBA_ERR_WORKSPACE;
   AttnArgs a = attn_args(d, s, q, k, v, index, o, false);
   a.lse = lse;
   const hipError_t e = ssba::launch_attn_bf16(a, d->head_dim, d->tile, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? SSBA_OK : SSBA_ERR_HIP;
+}
+
+ssba_status ssba_forward_train(const ssba_desc* d, const void* q, const void* k, const void* v,
+                               const int32_t* index, void* o, float* lse, void* stream) {
+  return ssba_forward_train_ex(d, q, k, v, index, kUnchecked, o, lse, stream);
 }
 
 ssba_status ssba_backward_workspace_size(const ssba_desc* d, size_t* scratch_bytes) {
@@ -346,9 +384,9 @@ ssba_status ssba_backward_workspace_size(const ssba_desc* d, size_t* scratch_byt
   return SSBA_OK;
 }
 
-ssba_status ssba_backward(const ssba_desc* d, const void* q, const void* k, const void* v, const void* o,
-                          const void* dout, const float* lse, const int32_t* index, void* dq, void* dk,
-                          void* dv, void* scratch, void* stream) {
+ssba_status ssba_backward_ex(const ssba_desc* d, const void* q, const void* k, const void* v, const void* o,
+                             const void* dout, const float* lse, const int32_t* index, size_t index_bytes,
+                             void* dq, void* dk, void* dv, void* scratch, size_t scratch_bytes, void* stream) {
   Shape s;
   const ssba_status st = check_desc(d, &s, false);
   if (st != SSBA_OK) return st;
@@ -361,6 +399,7 @@ ssba_status ssba_backward(const ssba_desc* d, const void* q, const void* k, cons
   if (!lse || !index || !scratch || !aligned(lse, 4) || !aligned(index, 4) || !aligned(scratch, 256))
     return SSBA_ERR_ARG;
   const BwdScratch w = bwd_scratch(d, s);
+  if (index_bytes < index_bytes_of(d, s) || scratch_bytes < w.total) return SSBA_ERR_WORKSPACE;
   ssba::BwdArgs a;
   std::memset(&a, 0, sizeof(a));
   a.q = q;
@@ -392,6 +431,13 @@ ssba_status ssba_backward(const ssba_desc* d, const void* q, const void* k, cons
   return e == hipSuccess ? SSBA_OK : SSBA_ERR_HIP;
 }
 
+ssba_status ssba_backward(const ssba_desc* d, const void* q, const void* k, const void* v, const void* o,
+                          const void* dout, const float* lse, const int32_t* index, void* dq, void* dk,
+                          void* dv, void* scratch, void* stream) {
+  return ssba_backward_ex(d, q, k, v, o, dout, lse, index, kUnchecked, dq, dk, dv, scratch, kUnchecked,
+                          stream);
+}
+
 ssba_status ssba_layers_workspace_size(const ssba_desc* d, int n_layers, size_t* index_bytes,
                                        size_t* scratch_bytes) {
   if (!d || n_layers < 1) return SSBA_ERR_ARG;
@@ -405,8 +451,9 @@ ssba_status ssba_layers_workspace_size(const ssba_desc* d, int n_layers, size_t*
   return SSBA_OK;
 }
 
-ssba_status ssba_forward_layers(const ssba_desc* d, const ssba_layer* layers, int n_layers,
-                                int32_t* index, void* scratch, void* stream) {
+ssba_status ssba_forward_layers_ex(const ssba_desc* d, const ssba_layer* layers, int n_layers,
+                                   int32_t* index, size_t index_bytes, void* scratch, size_t scratch_bytes,
+                                   void* stream) {
   if (!d || !layers || n_layers < 1) return SSBA_ERR_ARG;
   ssba_desc base = *d;
   if (is_topk(base.gate)) base.keep = 1;
@@ -424,8 +471,11 @@ ssba_status ssba_forward_layers(const ssba_desc* d, const ssba_layer* layers, in
       return SSBA_ERR_ARG;
     if (is_topk(d->gate) && (L.keep < 1 || L.keep > s.n_tiles)) return SSBA_ERR_ARG;
   }
-  const size_t idx_elems = index_bytes_of(&base, s) / sizeof(int32_t);
+  const size_t idx_bytes = index_bytes_of(&base, s);
+  const size_t idx_elems = idx_bytes / sizeof(int32_t);
   const size_t scr_stride = layer_scratch_stride(&base, s);
+  if (index_bytes / idx_bytes < (size_t)n_layers || scratch_bytes / scr_stride < (size_t)n_layers)
+    return SSBA_ERR_WORKSPACE;
   int cached[2] = {-1, -1};   // static gates: the layer whose index serves each parity
   for (int l = 0; l < n_layers; ++l) {
     const ssba_layer& L = layers[l];
@@ -439,23 +489,28 @@ ssba_status ssba_forward_layers(const ssba_desc* d, const ssba_layer* layers, in
     void* sl = static_cast<char*>(scratch) + (size_t)l * scr_stride;
     if (is_topk(d->gate)) {
       dl.keep = L.keep;
-      st = ssba_forward_topk(&dl, L.q, L.k, L.v, il, sl, L.o, stream);
+      st = ssba_forward_topk_ex(&dl, L.q, L.k, L.v, il, idx_bytes, sl, scr_stride, L.o, stream);
     } else {
       const int par = l & 1;
       if (cached[par] < 0) {
-        st = ssba_build_index(&dl, nullptr, nullptr, il, sl, stream);
+        st = ssba_build_index_ex(&dl, nullptr, nullptr, il, idx_bytes, sl, scr_stride, stream);
         if (st != SSBA_OK) return st;
         cached[par] = l;
       }
-      st = ssba_forward(&dl, L.q, L.k, L.v, index + (size_t)cached[par] * idx_elems, L.o, stream);
+      st = ssba_forward_ex(&dl, L.q, L.k, L.v, index + (size_t)cached[par] * idx_elems, idx_bytes, L.o, stream);
     }
     if (st != SSBA_OK) return st;
   }
   return SSBA_OK;
 }
 
-ssba_status ssba_read_device_status(const ssba_desc* d, const void* scratch, ssba_status* out,
-                                    void* stream) {
+ssba_status ssba_forward_layers(const ssba_desc* d, const ssba_layer* layers, int n_layers,
+                                int32_t* index, void* scratch, void* stream) {
+  return ssba_forward_layers_ex(d, layers, n_layers, index, kUnchecked, scratch, kUnchecked, stream);
+}
+
+ssba_status ssba_read_device_status_ex(const ssba_desc* d, const void* scratch, size_t scratch_bytes,
+                                       ssba_status* out, void* stream) {
   if (!d) return SSBA_ERR_ARG;
   ssba_desc base = *d;   // the flags do not depend on keep
   if (is_topk(base.gate) && base.keep < 1) base.keep = 1;
@@ -463,9 +518,10 @@ ssba_status ssba_read_device_status(const ssba_desc* d, const void* scratch, ssb
   const ssba_status st = check_desc(&base, &s);
   if (st != SSBA_OK) return st;
   if (!scratch || !out || !aligned(scratch, 8)) return SSBA_ERR_ARG;
+  if (scratch_bytes < scratch_bytes_of(&base, s)) return SSBA_ERR_WORKSPACE;
   const size_t n = (size_t)d->batch * d->heads * s.n_tiles;
   const int32_t* flags =
-      reinterpret_cast<const int32_t*>(static_cast<const char*>(scratch) + flags_offset_of(d, s));
+      reinterpret_cast<const int32_t*>(static_cast<const char*>(scratch) + flags_offset_of(&base, s));
   std::vector<int32_t> host(n);
   hipStream_t hs = static_cast<hipStream_t>(stream);
   if (hipMemcpyAsync(host.data(), flags, n * sizeof(int32_t), hipMemcpyDeviceToHost, hs) != hipSuccess)
@@ -475,6 +531,11 @@ ssba_status ssba_read_device_status(const ssba_desc* d, const void* scratch, ssb
   for (int32_t f : host) any |= f;
   *out = any ? SSBA_ERR_NONFINITE : SSBA_OK;
   return SSBA_OK;
+}
+
+ssba_status ssba_read_device_status(const ssba_desc* d, const void* scratch, ssba_status* out,
+                                    void* stream) {
+  return ssba_read_device_status_ex(d, scratch, kUnchecked, out, stream);
 }
 
 }  // extern "C"

@@ -385,16 +385,6 @@ hipError_t launch_t(const AttnArgs& a0, hipStream_t s) {
 
 }  // namespace
 
-const char* attn_kernel_name(const AttnArgs& a, int head_dim, int tile, int dtype) {
-  if (dtype == SSBA_DT_F32) return head_dim == 64 ? "k_attn_f32<64>" : "k_attn_f32<128>";
-  if (mfma_supported(head_dim, tile, a.dense != 0, a.n_tiles, a.seq, (int64_t)a.seq * a.st))
-    return mfma_kernel_name(head_dim, tile, a.dense != 0, a.gated != 0);
-  static const char* const names[2][3] = {
-      {"k_attn_bf16<64, 2>", "k_attn_bf16<64, 3>", "k_attn_bf16<64, 4>"},
-      {"k_attn_bf16<128, 2>", "k_attn_bf16<128, 3>", "k_attn_bf16<128, 4>"}};
-  return names[head_dim == 64 ? 0 : 1][tile == 4 ? 0 : tile == 8 ? 1 : 2];
-}
-
 hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, int tile, hipStream_t s) {
   if (mfma_supported(head_dim, tile, a.dense != 0, a.n_tiles, a.seq, (int64_t)a.seq * a.st))
     return launch_attn_mfma(a, head_dim, tile, s);

@@ -681,25 +681,6 @@ k_attn_mfma(AttnArgs a) {
 
 }  // namespace
 
-const char* mfma_kernel_name(int head_dim, int tile, bool dense, bool gated) {
-  static const char* const names[2][2][2] = {
-      {{"k_attn_mfma<64, 3, false, false>", "k_attn_mfma<64, 3, true, false>"},
-       {"k_attn_mfma<64, 4, false, false>", "k_attn_mfma<64, 4, true, false>"}},
-      {{"k_attn_mfma<128, 3, false, false>", "k_attn_mfma<128, 3, true, false>"},
-       {"k_attn_mfma<128, 4, false, false>", "k_attn_mfma<128, 4, true, false>"}}};
-  if (gated && !dense) return head_dim == 64 ? "k_attn_mfma<64, 3, false, true>" : "k_attn_mfma<128, 3, false, true>";
-  // The dense control runs natural-order rows only; it uses the 8x8 shape.
-  const int ti = (!dense && tile == 16) ? 1 : 0;
-  return names[head_dim == 64 ? 0 : 1][ti][dense ? 1 : 0];
-}
-
-bool mfma_supported(int head_dim, int tile, bool dense, int n_tiles, int seq, int64_t span) {
-  // 32-bit byte offsets inside one (batch, head); at most 64 kept blocks;
-  // natural-order chunks need at least one full chunk of rows.
-  return (head_dim == 64 || head_dim == 128) && (dense || ((tile == 8 || tile == 16) && n_tiles <= 64)) &&
-         seq >= KC && 2 * span < ((int64_t)1 << 32);
-}
-
 hipError_t launch_attn_mfma(const AttnArgs& a0, int head_dim, int tile, hipStream_t s) {
   AttnArgs a = a0;
   const int gpb = (tile == 16) ? 4 : 1;   // 64-query groups per image block

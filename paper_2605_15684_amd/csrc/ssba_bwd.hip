@@ -641,10 +641,6 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
 
 }  // namespace
 
-bool bwd_supported(int head_dim, int tile, int n_tiles, int dtype) {
-  return dtype == SSBA_DT_BF16 && (head_dim == 64 || head_dim == 128) && tile == 8 && n_tiles <= 64;
-}
-
 hipError_t launch_backward(const BwdArgs& a0, int head_dim, hipStream_t s) {
   BwdArgs a = a0;
   a.n_text_groups = (a.f.n_text + 63) / 64;

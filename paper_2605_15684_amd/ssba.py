@@ -95,6 +95,18 @@ def _stream(dev) -> int:
     return torch.cuda.current_stream(dev).cuda_stream
 
 
+def _nbytes(t: torch.Tensor) -> int:
+    return t.numel() * t.element_size()
+
+
+def _check_buffer(t: torch.Tensor, what: str, dtype=None) -> None:
+    """A workspace buffer must be a contiguous GPU tensor (its size is checked
+    by the library, which returns SSBA_ERR_WORKSPACE when it is short)."""
+    if not (isinstance(t, torch.Tensor) and t.is_cuda and t.is_contiguous()
+            and (dtype is None or t.dtype == dtype)):
+        raise ValueError(f"{what} must be a contiguous GPU tensor" + (f" of {dtype}" if dtype else ""))
+
+
 def alloc_workspace(desc, device) -> Tuple[torch.Tensor, torch.Tensor]:
     """Index (int32 [B, H, T_b, 1 + T_b]) and scratch buffers for `desc`."""
     ib, sb = _lib.workspace_size(desc)
@@ -114,14 +126,12 @@ def build_index(q, k, desc, index=None, scratch=None):
         dev = q.device if isinstance(q, torch.Tensor) else torch.device("cuda", torch.cuda.current_device())
     if index is None or scratch is None:
         index, scratch = alloc_workspace(desc, dev)
-    ib, sb = _lib.workspace_size(desc)
-    if not (index.is_cuda and scratch.is_cuda and index.dtype == torch.int32 and index.is_contiguous()
-            and index.numel() * 4 >= ib and scratch.numel() * scratch.element_size() >= sb):
-        raise ValueError("index / scratch buffers too small or not on the GPU")
+    _check_buffer(index, "index", torch.int32)
+    _check_buffer(scratch, "scratch")
     qp = q.data_ptr() if desc.gate in _TOPK else None
     kp = k.data_ptr() if desc.gate in _TOPK else None
-    _lib.check(_lib.build_index(desc, qp, kp, index.data_ptr(), scratch.data_ptr(), _stream(dev)),
-               "ssba_build_index")
+    _lib.check(_lib.build_index(desc, qp, kp, index.data_ptr(), scratch.data_ptr(), _stream(dev),
+                                _nbytes(index), _nbytes(scratch)), "ssba_build_index")
     return index, scratch
 
 
@@ -130,13 +140,9 @@ def forward(q, k, v, index, desc, out=None):
     if out is None:
         out = torch.empty_strided(q.shape, q.stride(), dtype=q.dtype, device=q.device)
     _check_tensors(desc, q, k, v, out)
-    if not (index.is_cuda and index.dtype == torch.int32 and index.is_contiguous()):
-        raise ValueError("index must be a contiguous int32 GPU tensor")
-    ib, _ = _lib.workspace_size(desc)
-    if index.numel() * 4 < ib:
-        raise ValueError("index buffer too small")
+    _check_buffer(index, "index", torch.int32)
     _lib.check(_lib.forward(desc, q.data_ptr(), k.data_ptr(), v.data_ptr(), index.data_ptr(),
-                            out.data_ptr(), _stream(q.device)), "ssba_forward")
+                            out.data_ptr(), _stream(q.device), _nbytes(index)), "ssba_forward")
     return out
 
 
@@ -161,12 +167,11 @@ def forward_topk(q, k, v, desc, index=None, scratch=None, out=None):
     _check_tensors(desc, q, k, v, out)
     if index is None or scratch is None:
         index, scratch = alloc_workspace(desc, q.device)
-    ib, sb = _lib.workspace_size(desc)
-    if not (index.is_cuda and scratch.is_cuda and index.dtype == torch.int32 and index.is_contiguous()
-            and index.numel() * 4 >= ib and scratch.numel() * scratch.element_size() >= sb):
-        raise ValueError("index / scratch buffers too small or not on the GPU")
+    _check_buffer(index, "index", torch.int32)
+    _check_buffer(scratch, "scratch")
     _lib.check(_lib.forward_topk(desc, q.data_ptr(), k.data_ptr(), v.data_ptr(), index.data_ptr(),
-                                 scratch.data_ptr(), out.data_ptr(), _stream(q.device)), "ssba_forward_topk")
+                                 scratch.data_ptr(), out.data_ptr(), _stream(q.device), _nbytes(index),
+                                 _nbytes(scratch)), "ssba_forward_topk")
     return index, scratch, out
 
 
@@ -197,12 +202,10 @@ def forward_layers(layers, desc, index=None, scratch=None):
         index = torch.empty((n, desc.batch, desc.heads, tb, tb + 1), dtype=torch.int32, device=dev)
     if scratch is None:
         scratch = torch.empty((n, sb // n // 8), dtype=torch.float64, device=dev)
-    if not (index.is_cuda and scratch.is_cuda and index.dtype == torch.int32 and index.is_contiguous()
-            and scratch.is_contiguous() and index.numel() * 4 >= ib
-            and scratch.numel() * scratch.element_size() >= sb):
-        raise ValueError("index / scratch buffers too small or not on the GPU")
-    _lib.check(_lib.forward_layers(desc, arr, index.data_ptr(), scratch.data_ptr(), _stream(dev)),
-               "ssba_forward_layers")
+    _check_buffer(index, "index", torch.int32)
+    _check_buffer(scratch, "scratch")
+    _lib.check(_lib.forward_layers(desc, arr, index.data_ptr(), scratch.data_ptr(), _stream(dev),
+                                   _nbytes(index), _nbytes(scratch)), "ssba_forward_layers")
     return index, scratch
 
 
@@ -216,8 +219,10 @@ def forward_train(q, k, v, index, desc, out=None, lse=None):
     _check_tensors(desc, q, k, v, out)
     if not (lse.is_cuda and lse.dtype == torch.float32 and lse.is_contiguous() and lse.shape == q.shape[:3]):
         raise ValueError("lse must be a contiguous fp32 GPU tensor of shape [B, H, T]")
+    _check_buffer(index, "index", torch.int32)
     _lib.check(_lib.forward_train(desc, q.data_ptr(), k.data_ptr(), v.data_ptr(), index.data_ptr(),
-                                  out.data_ptr(), lse.data_ptr(), _stream(q.device)), "ssba_forward_train")
+                                  out.data_ptr(), lse.data_ptr(), _stream(q.device), _nbytes(index)),
+               "ssba_forward_train")
     return out, lse
 
 
@@ -230,15 +235,19 @@ def backward(q, k, v, out, dout, lse, index, desc, dq=None, dk=None, dv=None, sc
     if scratch is None:
         sb = _lib.backward_workspace_size(desc)
         scratch = torch.empty(((sb + 7) // 8,), dtype=torch.float64, device=q.device)
+    _check_buffer(index, "index", torch.int32)
+    _check_buffer(scratch, "scratch")
     _lib.check(_lib.backward(desc, q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), dout.data_ptr(),
                              lse.data_ptr(), index.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
-                             scratch.data_ptr(), _stream(q.device)), "ssba_backward")
+                             scratch.data_ptr(), _stream(q.device), _nbytes(index), _nbytes(scratch)),
+               "ssba_backward")
     return dq, dk, dv
 
 
 def read_status(desc, scratch) -> int:
     """Synchronize and return SSBA_OK or SSBA_ERR_NONFINITE from the last gate."""
-    return _lib.read_device_status(desc, scratch.data_ptr(), _stream(scratch.device))
+    _check_buffer(scratch, "scratch")
+    return _lib.read_device_status(desc, scratch.data_ptr(), _stream(scratch.device), _nbytes(scratch))
 
 
 def attention(q, k, v, *, grid, tile, shift=None, layer=None, rho=None, keep=None, gate="topk",

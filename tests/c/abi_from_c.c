@@ -61,6 +61,20 @@ int main(void) {
   CHECK(ssba_build_index(&d, NULL, NULL, NULL, NULL, NULL) == SSBA_ERR_ARG);
   CHECK(ssba_forward(NULL, NULL, NULL, NULL, NULL, NULL, NULL) == SSBA_ERR_ARG);
   CHECK(ssba_forward_kernel(&d, 0) != NULL);
+
+  /* short workspaces are rejected before any launch (the pointers are never
+   * dereferenced: the size check precedes every launch) */
+  {
+    void* fake = (void*)(uintptr_t)0x100000;
+    size_t ib = 0, sb = 0;
+    CHECK(ssba_workspace_size(&d, &ib, &sb) == SSBA_OK);
+    CHECK(ssba_build_index_ex(&d, fake, fake, (int32_t*)fake, ib - 1, fake, sb, NULL) == SSBA_ERR_WORKSPACE);
+    CHECK(ssba_build_index_ex(&d, fake, fake, (int32_t*)fake, ib, fake, sb - 1, NULL) == SSBA_ERR_WORKSPACE);
+    CHECK(ssba_forward_ex(&d, fake, fake, fake, (const int32_t*)fake, ib - 1, fake, NULL) == SSBA_ERR_WORKSPACE);
+    CHECK(ssba_forward_topk_ex(&d, fake, fake, fake, (int32_t*)fake, ib, fake, sb - 1, fake, NULL) ==
+          SSBA_ERR_WORKSPACE);
+    CHECK(ssba_forward_topk_ex(&d, NULL, fake, fake, (int32_t*)fake, ib, fake, sb, fake, NULL) == SSBA_ERR_ARG);
+  }
   CHECK(ssba_forward_kernel(&d, 7) == NULL);
 
   /* the Haar pair and the probe reject bad arguments the same way */

@@ -1,0 +1,40 @@
+// Recording stand-ins for the kernel launchers of the SSBA library, for a CPU
+// build of its host layer (argument checks, workspace arithmetic, dispatch,
+// the layer-stack driver) under AddressSanitizer and
+// UndefinedBehaviorSanitizer.  Each records what it was given and launches
+// nothing.
+#include "ssba_common.h"
+#include "stub_log.h"
+
+std::vector<StubCall>& stub_calls() {
+  static std::vector<StubCall> calls;
+  return calls;
+}
+
+namespace ssba {
+
+namespace {
+hipError_t rec_index(const char* what, const IndexArgs& a) {
+  stub_calls().push_back({what, a.index, a.qb, a.flags, nullptr, a.keep, a.f.sy, a.f.sx, 0});
+  return hipSuccess;
+}
+hipError_t rec_attn(const char* what, const AttnArgs& a) {
+  stub_calls().push_back({what, a.gated ? a.index_out : a.index, a.qb, a.flags, a.o, a.keep, a.f.sy, a.f.sx,
+                          a.gated});
+  return hipSuccess;
+}
+}  // namespace
+
+hipError_t launch_pool(const IndexArgs& a, int, hipStream_t) { return rec_index("pool", a); }
+hipError_t launch_gate_topk(const IndexArgs& a, hipStream_t) { return rec_index("gate_topk", a); }
+hipError_t launch_gate_topk_shared(const IndexArgs& a, hipStream_t) { return rec_index("gate_shared", a); }
+hipError_t launch_gate_static(const IndexArgs& a, int, hipStream_t) { return rec_index("gate_static", a); }
+hipError_t launch_attn_bf16(const AttnArgs& a, int, int, hipStream_t) { return rec_attn("attn_bf16", a); }
+hipError_t launch_attn_f32(const AttnArgs& a, int, int, hipStream_t) { return rec_attn("attn_f32", a); }
+hipError_t launch_attn_mfma(const AttnArgs& a, int, int, hipStream_t) { return rec_attn("attn_mfma", a); }
+hipError_t launch_backward(const BwdArgs& a, int, hipStream_t) {
+  stub_calls().push_back({"backward", a.index, a.lse2, a.kmask, a.dq, 0, a.f.sy, a.f.sx, 0});
+  return hipSuccess;
+}
+
+}  // namespace ssba

@@ -1,0 +1,15 @@
+// Call log of the recording launcher stand-ins (tests/sanitize/stub_launch.cpp).
+#pragma once
+
+#include <vector>
+
+struct StubCall {
+  const char* what;       // launcher name
+  const void* index;      // index read or written
+  const void* scratch;    // first scratch region (pooled q sums, backward lse2)
+  const void* flags;      // status flags (gates) / kept-block masks (backward)
+  const void* out;        // attention output
+  int keep, sy, sx, gated;
+};
+
+std::vector<StubCall>& stub_calls();

@@ -36,7 +36,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.ssba_abi_version() == 2
+    assert lib.ssba_abi_version() == 3
     seen = set()
     for s in range(7):
         txt = _lib.status_str(s)
@@ -277,3 +277,36 @@ def test_probe_rejects_bad_arguments(lib):
     assert _lib.probe_mfma(4, 0, sink, None) == _lib.SSBA_ERR_ARG
     assert _lib.probe_mfma(4, (1 << 20) + 1, sink, None) == _lib.SSBA_ERR_ARG
     assert _lib.probe_mfma(4, 10, None, None) == _lib.SSBA_ERR_ARG
+
+
+def test_short_workspace_rejected_before_launch(lib):
+    """The _ex entry points return SSBA_ERR_WORKSPACE, before anything is
+    launched, when index or scratch is one byte short of what the workspace
+    queries report (no device is touched: the check precedes every launch)."""
+    fake = ctypes.c_void_p(0x100000)
+    d = _desc()
+    ib, sb = _lib.workspace_size(d)
+    W = _lib.SSBA_ERR_WORKSPACE
+    assert _lib.build_index(d, fake, fake, fake, fake, None, ib - 1, sb) == W
+    assert _lib.build_index(d, fake, fake, fake, fake, None, ib, sb - 1) == W
+    assert _lib.forward(d, fake, fake, fake, fake, fake, None, ib - 1) == W
+    assert _lib.forward_topk(d, fake, fake, fake, fake, fake, fake, None, ib - 1, sb) == W
+    assert _lib.forward_topk(d, fake, fake, fake, fake, fake, fake, None, ib, sb - 1) == W
+    assert _lib.forward_train(d, fake, fake, fake, fake, fake, fake, None, ib - 1) == W
+    bsb = _lib.backward_workspace_size(d)
+    assert _lib.backward(d, *([fake] * 11), None, ib - 1, bsb) == W
+    assert _lib.backward(d, *([fake] * 11), None, ib, bsb - 1) == W
+    out = ctypes.c_int(0)
+    assert lib.ssba_read_device_status_ex(ctypes.byref(d), fake, sb - 1, ctypes.byref(out), None) == W
+    # the layer stack needs n_layers slices of each
+    layers = (_lib.SsbaLayer * 3)()
+    for e in layers:
+        e.q = e.k = e.v = e.o = 0x100000
+        e.keep = 10
+    lib_, lsb = _lib.layers_workspace_size(d, 3)
+    assert _lib.forward_layers(d, layers, fake, fake, None, lib_ - 1, lsb) == W
+    assert _lib.forward_layers(d, layers, fake, fake, None, lib_, lsb - 1) == W
+    # the argument checks still come first
+    assert _lib.forward_topk(d, None, fake, fake, fake, fake, fake, None, 0, 0) == _lib.SSBA_ERR_ARG
+    bad = _desc(keep=0)
+    assert _lib.build_index(bad, fake, fake, fake, fake, None, 0, 0) == _lib.SSBA_ERR_ARG
