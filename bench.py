@@ -15,9 +15,12 @@ a HIP graph captured from the same calls (same kernels, same work; the replay
 is checked bit-exact against the eager output); `value` uses the faster.
 Index, forward and dense launches, and the two-call form, are also timed
 separately, back to back: five rounds that time each form in turn, median
-per form.  The default warm-up (1000 steps) is long enough for the clock to
-settle under load: shorter ones leave the first timed milliseconds 10-15 %
-slow.
+per form.  Before the warm-up steps, a clock-settle phase runs the step back
+to back for --settle-ms milliseconds of wall time (default 100): the GPU
+clock needs about 10 ms of load to reach its steady state, and without the
+phase the first timed milliseconds run 10-15 % slow.  The phase is reported
+in the output line (clock_settle_ms, clock_settle_calls); --settle-ms 0
+switches it off.
 These are warm numbers (Q, K, V and O stay in the 256 MB MALL between
 calls); ms_step_cold and ms_fwd_cold are the median of ten single calls each
 made after a 1 GiB buffer is written, so the inputs come from HBM.  Prints
@@ -237,6 +240,19 @@ class Runner:
         return ms, g
 
 
+def cpu_model() -> str:
+    """Host CPU model name from /proc/cpuinfo (platform's processor string
+    otherwise)."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
 def cpu_baseline(runner, budget_s: float = 12.0) -> dict:
     """The fp64 oracle on the same inputs: the gate for every (batch, head),
     then attention head by head until the time budget is spent."""
@@ -271,13 +287,28 @@ def cpu_baseline(runner, budget_s: float = 12.0) -> dict:
             "kind": "oracle",
             "sample": f"fp64 oracle: gate for all {n_bh} (batch, head) pairs "
                       f"({t_index:.2f} s, pro-rated), attention for {done} of {n_bh} pairs "
-                      f"({t_attn:.2f} s); host {platform.processor() or platform.machine()}, "
-                      f"os.cpu_count()={os.cpu_count()}",
+                      f"({t_attn:.2f} s); host {cpu_model()}, os.cpu_count()={os.cpu_count()}",
+            "cpu_model": cpu_model(),
             "seconds": round(t_index + t_attn, 3)}
 
 
-def measure(w, steps: int, warmup: int, dense_steps: int, graph: bool = True):
+def settle_clock(fn, ms: float) -> int:
+    """Run `fn` back to back for `ms` milliseconds of wall time (synchronizing
+    every 50 calls); returns the number of calls."""
+    import torch
+    calls = 0
+    t0 = time.perf_counter()
+    while (time.perf_counter() - t0) * 1e3 < ms:
+        for _ in range(50):
+            fn()
+        calls += 50
+        torch.cuda.synchronize()
+    return calls
+
+
+def measure(w, steps: int, warmup: int, dense_steps: int, graph: bool = True, settle_ms: float = 0.0):
     r = Runner(w)
+    settle_calls = settle_clock(r.step, settle_ms) if settle_ms > 0 else 0
     for _ in range(warmup):
         r.step()
     wall_ms, step_ms = r.timed_steps(steps)
@@ -315,6 +346,7 @@ def measure(w, steps: int, warmup: int, dense_steps: int, graph: bool = True):
         "tflops_step": f / (best_ms * 1e-3) / 1e12,
         "tflops_dense": flops(w, dense=True) / (dense_ms * 1e-3) / 1e12,
         "speedup_kernel": dense_ms / fwd_ms, "speedup_step": dense_ms / best_ms,
+        "settle_calls": settle_calls,
     }
 
 
@@ -576,7 +608,9 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--settle-ms", type=float, default=100.0,
+                    help="clock-settle phase before the warm-up: back-to-back steps for this long")
     ap.add_argument("--workload", default="grid64")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--sweep", action="store_true")
@@ -615,7 +649,7 @@ def main():
     if args.layers:
         print(json.dumps(measure_layers(w, max(5, args.steps // 10), max(2, args.warmup // 10))), flush=True)
         return
-    r, m = measure(w, args.steps, args.warmup, max(20, args.steps // 4))
+    r, m = measure(w, args.steps, args.warmup, max(20, args.steps // 4), settle_ms=args.settle_ms)
     f = flops(w)
     achieved = f / (m["ms_fwd"] * 1e-3) / 1e12
     from paper_2605_15684_amd import _lib
@@ -631,6 +665,7 @@ def main():
         "metric": "SSBA fwd ms/call + effective TFLOP/s (% bf16 MFMA peak) at 4096 tokens, 84% sparse",
         "value": round(m["tflops_step"], 2), "unit": "TFLOP/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "clock_settle_ms": args.settle_ms, "clock_settle_calls": m["settle_calls"],
         "ms_per_step": round(m["ms_step"], 5), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"{w.name}: {describe(w)}", "global_batch": w.batch,
@@ -659,7 +694,7 @@ def main():
         for c in cases:
             del r
             torch.cuda.empty_cache()
-            r, mm = measure(c, max(20, args.steps // 2), args.warmup, 20, graph=False)
+            r, mm = measure(c, max(20, args.steps // 2), args.warmup, 20, graph=False, settle_ms=args.settle_ms)
             print(json.dumps({"workload": c.name, "desc": describe(c),
                               **{k: (None if v is None else round(v, 5)) for k, v in mm.items()},
                               "pct_peak_fwd": round(100 * mm["tflops_fwd"] / PEAK_BF16_TFLOPS, 2)}),
