@@ -322,16 +322,17 @@ ssba_status ssba_forward_topk_ex(const ssba_desc* d, const void* q, const void* 
     st = ssba_build_index_ex(d, q, k, index, index_bytes, scratch, scratch_bytes, stream);
     return st != SSBA_OK ? st : ssba_forward_ex(d, q, k, v, index, index_bytes, o, stream);
   }
+  // Pooled key sums, then the attention kernel, which forms each block's
+  // pooled query sum from its own Q rows, gates the block and attends.
   IndexArgs ia = index_args(d, s, q, k, index, scratch);
   AttnArgs aa = attn_args(d, s, q, k, v, nullptr, o, false);
   aa.gated = 1;
   aa.keep = d->keep;
-  aa.qb = ia.qb;
   aa.kb = ia.kb;
   aa.index_out = index;
   aa.flags = ia.flags;
   hipStream_t hs = static_cast<hipStream_t>(stream);
-  hipError_t e = ssba::launch_pool(ia, d->dtype, hs);
+  hipError_t e = ssba::launch_pool_keys(ia, hs);
   if (e == hipSuccess) e = ssba::launch_attn_bf16(aa, d->head_dim, d->tile, hs);
   return e == hipSuccess ? SSBA_OK : SSBA_ERR_HIP;
 }

@@ -172,19 +172,24 @@ __device__ __forceinline__ double affinity(const double* qsum, const char* b0, c
 // Compression / Affinity Matrix / Top-k Gating; Algorithm 1 pool, affinity and
 // top-k steps), with the arithmetic of the separate gate kernels so the index
 // rows are bit-identical to theirs:
-//   1. the head's pooled key sums [D][T_b] are copied into the four K/V
-//      buffers (a quarter of the channels each; they are free until the
-//      first chunk is copied);
-//   2. threads c < D fetch channel c of the block's pooled query sum (the
-//      pool kernel of the same call wrote both sums);
+//   1. the head's pooled key sums [D][T_b] (written by the pooling pre-pass of
+//      the same call) are copied into the four K/V buffers (a quarter of the
+//      channels each; they are free until the first chunk is copied);
+//   2. the block's pooled query sum (Eq. 1) is formed here from the Q
+//      fragments the workgroup already holds: the two waves that hold the
+//      block's 64 query rows (slots 0-31 and 32-63) stage them through LDS,
+//      32 rows at a time, and thread c < D adds channel c of the slots in
+//      slot order in fp64 -- the pooling kernel's order and arithmetic
+//      (bf16 -> fp32 is exact), so the sum is the same to the bit;
 //   3. wave 0, lane j < T_b: S[i][j] = sum over channels, in order, of the
 //      rounded products; then the wave's radix select picks the keep largest.
 // Writes the index row and status flag of block i; returns the kept count
 // with the ids in gate_list.  Every wave of the workgroup calls it.
-template <int D>
-__device__ __forceinline__ int gate_block(const AttnArgs& a, int bh, int i, int w, int lane,
+template <int D, int NKS>
+__device__ __forceinline__ int gate_block(const AttnArgs& a, int bh, int i, int w, int lane, const bf16x8 (&qf)[NKS],
                                           char* b0, char* b1, char* b2, char* b3) {
   __shared__ double qsum[D];
+  __shared__ __attribute__((aligned(16))) char qstage[32 * 2 * D];   // 32 query rows
   const int tb = a.n_tiles;
   const int quarter_bytes = 2 * D * tb;   // D * tb * 8 / 4
   // 1. pooled key sums of this (batch, head): wave w copies quarter w.
@@ -199,10 +204,30 @@ __device__ __forceinline__ int gate_block(const AttnArgs& a, int bh, int i, int 
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(dst + o), 16,
                                                (unsigned)(w * quarter_bytes + o + 16 * lane), 0u, 0, 0);
   }
-  // 2. pooled query sums of block i, channel c = thread id.
+  // 2. pooled query sum of block i: channel c = thread id, slots in order.
   const int tid = 64 * w + lane;
-  if (tid < D) qsum[tid] = a.qb[((int64_t)bh * tb + i) * D + tid];
-  __builtin_amdgcn_s_waitcnt(0x0F70);
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // the Q fragments and the copies have landed
+  double qacc = 0.0;
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    if (w == half) {   // wave half (key stream 0) holds slots 32 half .. 32 half + 31
+      const int row = lane & 31, hw = lane >> 5;
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks)
+        *reinterpret_cast<bf16x8*>(qstage + row * 2 * D + 32 * ks + 16 * hw) = qf[ks];
+    }
+    __syncthreads();
+    if (tid < D) {
+      float xs[32];
+#pragma unroll
+      for (int r = 0; r < 32; ++r)
+        xs[r] = __uint_as_float((uint32_t)*reinterpret_cast<const uint16_t*>(qstage + r * 2 * D + 2 * tid) << 16);
+#pragma unroll
+      for (int r = 0; r < 32; ++r) qacc = (half == 0 && r == 0) ? (double)xs[r] : __dadd_rn(qacc, (double)xs[r]);
+    }
+    __syncthreads();
+  }
+  if (tid < D) qsum[tid] = qacc;
   __syncthreads();
   // 3. affinity row and ranking (wave 0).
   if (w == 0) {
@@ -314,7 +339,7 @@ k_attn_mfma(AttnArgs a) {
     load_q<NKS>(qf, qbase, qrow, st, hw);   // in flight during the gate or the list read
     int count, e;
     if constexpr (GATED) {
-      count = gate_block<D>(a, bh, i, w, lane, kA, kB, vA, vB);
+      count = gate_block<D, NKS>(a, bh, i, w, lane, qf, kA, kB, vA, vB);
       e = lane < count ? gate_list[lane] : 0;
     } else {
       // The count and the entries are requested together (one round trip).
@@ -602,16 +627,21 @@ k_attn_mfma(AttnArgs a) {
       lo_c = cn.lo;
       hi_c = cn.hi;
     } else {
-      // No next chunk: the same number of copies, every one past the end of
-      // the buffer range (no memory traffic; zeros land in kn, unread), so
-      // the wait below counts the same on every path.
+      // No next chunk: the same number of copies through a buffer resource
+      // with no records, so every one is out of range (no memory traffic;
+      // zeros land in kn, unread) and the wait below counts the same on
+      // every path.
       cn.row0 = 0;
       cn.rstep = 0;
       cn.y0 = 0;
 #pragma unroll
-      for (int mm = 0; mm < NIW; ++mm) cn.lane_off[mm] = 0x80000000u;
+      for (int mm = 0; mm < NIW; ++mm) cn.lane_off[mm] = 0;
     }
-    copy(rk, cn, kn, true);
+    // (The resource is built here, record count chosen by `more`: a choice
+    // between two resource variables would put them in memory.)
+    const __amdgpu_buffer_rsrc_t rkn = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<u16*>(kbase), (short)0, more ? (int)slice_bytes : 0, kRawBufferFlags);
+    copy(rkn, cn, kn, true);
     scores(kt, lo, hi);
     // Chunk c's V (copied before chunk c + 1's K) has landed in every wave.
     __builtin_amdgcn_s_waitcnt(kWaitVm0 | NIW);

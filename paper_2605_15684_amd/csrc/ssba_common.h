@@ -88,7 +88,6 @@ struct AttnArgs {
   // from the pooled sums and write the index rows and status flags.
   int gated;
   int keep;
-  const double* qb;      // [B][H][T_b][D] pooled query sums
   const double* kb;      // [B][H][D][T_b] pooled key sums
   int32_t* index_out;    // [B][H][T_b][1 + T_b]
   int32_t* flags;        // [B][H][T_b]
@@ -137,6 +136,9 @@ struct BwdArgs {
 
 // Launchers (each returns hipGetLastError() of its launch).
 hipError_t launch_pool(const IndexArgs& a, int dtype, hipStream_t s);
+// Pooled key sums only (bf16, 8x8 blocks): the pre-pass of the gated attention
+// kernel, which forms the pooled query sums itself.
+hipError_t launch_pool_keys(const IndexArgs& a, hipStream_t s);
 hipError_t launch_gate_topk(const IndexArgs& a, hipStream_t s);
 // Head-shared top-k gate: per-head affinity rows, then their sum over heads.
 hipError_t launch_gate_topk_shared(const IndexArgs& a, hipStream_t s);

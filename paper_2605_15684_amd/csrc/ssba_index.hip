@@ -38,22 +38,21 @@ __device__ __forceinline__ void unit_of(const IndexArgs& a, int& t, int& h, int&
   h = bh - b * a.heads;
 }
 
-// Block pooling.  One workgroup pools Q and K of one block.  The block's rows
-// are staged in LDS, up to 64 slots at a time, by all 256 threads with wide
-// loads; then 2 * D threads (one per channel of Q and of K) add the staged
-// slots in slot order in fp64, the ordered sum that makes the lists exact.
-// Pooled q is stored block-major [B][H][T_b][D]; pooled k channel-major
-// [B][H][D][T_b], so that the gate reads one channel of all key blocks with
-// one coalesced load.
-template <int DTYPE, int TILE_LOG2, int D>
+// Block pooling.  One workgroup pools Q and K (NT = 2), or K alone (NT = 1),
+// of one block.  The block's rows are staged in LDS, up to 64 slots at a
+// time, by all 256 threads with wide loads; then NT * D threads (one per
+// channel of each tensor) add the staged slots in slot order in fp64, the
+// ordered sum that makes the lists exact.  Pooled q is stored block-major
+// [B][H][T_b][D]; pooled k channel-major [B][H][D][T_b], so that the gate
+// reads one channel of all key blocks with one coalesced load.
+template <int DTYPE, int TILE_LOG2, int D, int NT>
 __global__ void __launch_bounds__(256) k_pool(IndexArgs a) {
   constexpr int SLOTS = 1 << (2 * TILE_LOG2);
   constexpr int SB = SLOTS < 64 ? SLOTS : 64;          // slots per stage
   constexpr bool BF16 = DTYPE == SSBA_DT_BF16;
   constexpr int EPV = BF16 ? 8 : 1;                    // elements per load
   constexpr int VPR = D / EPV;                         // loads per token row
-  constexpr int NT = 2;                                // tensors pooled
-  constexpr int LOADS = NT * SB * VPR;                 // per stage, Q then K
+  constexpr int LOADS = NT * SB * VPR;                 // per stage, (Q then) K
   using Vec = typename std::conditional<BF16, uint4, float>::type;
   __shared__ Vec stage[LOADS];
   int t, h, b;
@@ -72,7 +71,7 @@ __global__ void __launch_bounds__(256) k_pool(IndexArgs a) {
       const int tensor = idx / (SB * VPR), rem = idx % (SB * VPR);
       const int slot = rem / VPR, part = rem % VPR;
       const int64_t off = base + (int64_t)frame_row(a.f, t, s0 + slot) * a.st + part * EPV;
-      const void* src = tensor == 0 ? a.q : a.k;
+      const void* src = (NT == 2 && tensor == 0) ? a.q : a.k;
       v[r] = *reinterpret_cast<const Vec*>(static_cast<const char*>(src) + off * (BF16 ? 2 : 4));
     }
 #pragma unroll
@@ -101,7 +100,7 @@ __global__ void __launch_bounds__(256) k_pool(IndexArgs a) {
   }
   if (tid < NT * D) {
     const int64_t bh = (int64_t)b * a.heads + h;
-    if (which == 0)
+    if (NT == 2 && which == 0)
       a.qb[(bh * a.n_tiles + t) * D + c] = sum;
     else
       a.kb[(bh * D + c) * a.n_tiles + t] = sum;
@@ -286,9 +285,9 @@ template <int DTYPE, int D>
 void launch_pool_d(const IndexArgs& a, hipStream_t s) {
   dim3 grid(a.n_tiles * a.heads * a.batch), block(256);
   switch (a.f.tile_log2) {
-    case 2: hipLaunchKernelGGL((k_pool<DTYPE, 2, D>), grid, block, 0, s, a); break;
-    case 3: hipLaunchKernelGGL((k_pool<DTYPE, 3, D>), grid, block, 0, s, a); break;
-    default: hipLaunchKernelGGL((k_pool<DTYPE, 4, D>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((k_pool<DTYPE, 2, D, 2>), grid, block, 0, s, a); break;
+    case 3: hipLaunchKernelGGL((k_pool<DTYPE, 3, D, 2>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((k_pool<DTYPE, 4, D, 2>), grid, block, 0, s, a); break;
   }
 }
 
@@ -305,6 +304,14 @@ hipError_t launch_pool(const IndexArgs& a, int dtype, hipStream_t s) {
     launch_pool_t<SSBA_DT_F32>(a, s);
   else
     launch_pool_t<SSBA_DT_BF16>(a, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_pool_keys(const IndexArgs& a, hipStream_t s) {
+  if (a.f.tile_log2 != 3) return hipErrorInvalidValue;   // 8x8 blocks (the gated attention kernel)
+  dim3 grid(a.n_tiles * a.heads * a.batch), block(256);
+  if (a.head_dim == 64) hipLaunchKernelGGL((k_pool<SSBA_DT_BF16, 3, 64, 1>), grid, block, 0, s, a);
+  else hipLaunchKernelGGL((k_pool<SSBA_DT_BF16, 3, 128, 1>), grid, block, 0, s, a);
   return hipGetLastError();
 }
 

@@ -124,6 +124,9 @@ int main() {
     CHECK(ssba_forward_topk_ex(&d, b.q.data(), b.k.data(), b.v.data(), idx, ib, scr, sb, b.o.data(), nullptr) ==
           SSBA_OK);
     CHECK(stub_calls().size() == 2 && stub_calls()[1].gated == 1 && stub_calls()[1].index == idx);
+    // the fused call pools the keys only; the attention kernel gets their sums
+    CHECK(std::strcmp(stub_calls()[0].what, "pool_keys") == 0);
+    CHECK(stub_calls()[1].scratch == static_cast<char*>(scr) + (size_t)8 * 16 * 64 * 64);
 
     // misaligned and missing pointers
     CHECK(ssba_forward_ex(&d, static_cast<char*>(static_cast<void*>(b.q.data())) + 2, b.k.data(), b.v.data(), idx,

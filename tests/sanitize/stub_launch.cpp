@@ -19,13 +19,14 @@ hipError_t rec_index(const char* what, const IndexArgs& a) {
   return hipSuccess;
 }
 hipError_t rec_attn(const char* what, const AttnArgs& a) {
-  stub_calls().push_back({what, a.gated ? a.index_out : a.index, a.qb, a.flags, a.o, a.keep, a.f.sy, a.f.sx,
+  stub_calls().push_back({what, a.gated ? a.index_out : a.index, a.kb, a.flags, a.o, a.keep, a.f.sy, a.f.sx,
                           a.gated});
   return hipSuccess;
 }
 }  // namespace
 
 hipError_t launch_pool(const IndexArgs& a, int, hipStream_t) { return rec_index("pool", a); }
+hipError_t launch_pool_keys(const IndexArgs& a, hipStream_t) { return rec_index("pool_keys", a); }
 hipError_t launch_gate_topk(const IndexArgs& a, hipStream_t) { return rec_index("gate_topk", a); }
 hipError_t launch_gate_topk_shared(const IndexArgs& a, hipStream_t) { return rec_index("gate_shared", a); }
 hipError_t launch_gate_static(const IndexArgs& a, int, hipStream_t) { return rec_index("gate_static", a); }

@@ -6,7 +6,7 @@
 struct StubCall {
   const char* what;       // launcher name
   const void* index;      // index read or written
-  const void* scratch;    // first scratch region (pooled q sums, backward lse2)
+  const void* scratch;    // pooled sums (q for the gates, k for the attention), backward lse2
   const void* flags;      // status flags (gates) / kept-block masks (backward)
   const void* out;        // attention output
   int keep, sy, sx, gated;
