@@ -219,6 +219,26 @@ ssba_status ssba_backward_ex(const ssba_desc* d, const void* q, const void* k, c
                              void* dq, void* dk, void* dv, void* scratch, size_t scratch_bytes,
                              void* hip_stream);
 
+/* Largest scratch (bytes) that ssba_forward_topk_noalloc provides: the
+ * fixed device array it uses in place of a caller buffer. */
+#define SSBA_NOALLOC_SCRATCH_BYTES ((size_t)8 << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops, harnesses that forbid hipMalloc): the same call
+ * and results as ssba_forward_topk, with the scratch taken from a fixed array
+ * of SSBA_NOALLOC_SCRATCH_BYTES in device memory that the library holds on
+ * every device it runs on until the process ends.  The caller still passes
+ * the inputs and the outputs (`index`, `index_bytes`, `o`).  Returns
+ * SSBA_ERR_WORKSPACE, before anything is launched, when the scratch that
+ * ssba_workspace_size reports for `d` exceeds SSBA_NOALLOC_SCRATCH_BYTES, or
+ * when `index_bytes` is short.  Allocates nothing.  Every call on one device
+ * shares that device's array: calls that overlap on a device (several
+ * streams or threads) race; calls ordered on one stream do not.  The status
+ * flags of the gate stay in the array, so ssba_read_device_status has no
+ * buffer to read for this call. */
+ssba_status ssba_forward_topk_noalloc(const ssba_desc* d, const void* q, const void* k, const void* v,
+                                      int32_t* index, size_t index_bytes, void* o, void* hip_stream);
+
 /* One layer of a stack run by ssba_forward_layers. */
 typedef struct ssba_layer {
   const void* q;    /* this layer's Q, K, V and output O (layout of the descriptor) */

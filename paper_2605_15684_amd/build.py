@@ -31,6 +31,7 @@ SOURCES = {
     "ssba_haar.hip": ["-ffp-contract=off"],
     "ssba_bwd.hip": [],
     "ssba_probe.hip": [],
+    "ssba_noalloc.hip": [],
 }
 
 COMMON = [

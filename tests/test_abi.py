@@ -310,3 +310,17 @@ def test_short_workspace_rejected_before_launch(lib):
     assert _lib.forward_topk(d, None, fake, fake, fake, fake, fake, None, 0, 0) == _lib.SSBA_ERR_ARG
     bad = _desc(keep=0)
     assert _lib.build_index(bad, fake, fake, fake, fake, None, 0, 0) == _lib.SSBA_ERR_ARG
+
+
+def test_noalloc_rejects_scratch_beyond_its_array(lib):
+    """ssba_forward_topk_noalloc returns SSBA_ERR_WORKSPACE, before touching a
+    device, when the descriptor's scratch exceeds the fixed array, and
+    SSBA_ERR_ARG for a gate without scratch sums."""
+    fake = 0x100000
+    d = _desc(batch=8, heads=32, head_dim=128)
+    _, sb = _lib.workspace_size(d)
+    assert sb > _lib.NOALLOC_SCRATCH_BYTES
+    assert _lib.forward_topk_noalloc(d, fake, fake, fake, fake, fake, None, 1 << 30) == _lib.SSBA_ERR_WORKSPACE
+    w = _desc(gate=_lib.GATE_WINDOW, win_h=2, win_w=2)
+    assert _lib.forward_topk_noalloc(w, fake, fake, fake, fake, fake, None, 1 << 30) == _lib.SSBA_ERR_ARG
+    assert lib.ssba_forward_topk_noalloc(None, fake, fake, fake, fake, 1 << 30, fake, None) == _lib.SSBA_ERR_ARG
