@@ -31,14 +31,17 @@ Flops are counted over computed (kept) query/key pairs only: 4 * D per pair
 (2 * D for Q K^T, 2 * D for P V).  Pairs per (batch, head):
 T_img * (keep * Bt^2 + T_txt) + T_txt * T.
 
-The roofline object describes the attention kernel (the dominant one) as
-ssba_forward launches it alone (the gated launch inside ssba_forward_topk is
-the same kernel template plus the gate prologue and cannot be timed apart):
-its flops per launch over its average launch time (HIP events on the stream
-it runs on).  `traffic` is the HBM traffic per launch measured with rocprofv3
-counters (FETCH_SIZE and WRITE_SIZE, scaled by what the same counters read
-for a plain copy of known size), reported only while the kernel's sources
-still hash to the values the counters were taken on.
+The roofline object describes the step's dominant kernel: the gated
+attention launch of ssba_forward_topk (the attention kernel with the top-k
+gate of each query block in its prologue), timed alone through
+ssba_forward_gated_ex on the pooled key sums the step's pooling launch left
+in the scratch: its flops per launch over its average launch time (HIP
+events on the stream it runs on).  roofline_ungated gives the same for the
+attention kernel as ssba_forward launches it (index read, no gate), and
+ms_pool the pooling launch alone.  `traffic` is the HBM traffic per launch
+measured with rocprofv3 counters (FETCH_SIZE and WRITE_SIZE, scaled by what
+the same counters read for a plain copy of known size), reported only while
+the kernel's sources still hash to the values the counters were taken on.
 
 --layers prints instead one JSON line for a 24-layer stack through
 ssba_forward_layers (synthetic per-layer keep schedule averaging 84.18 %
@@ -87,8 +90,11 @@ MEASURED_TRAFFIC = {
     ("k_haar_dwt<unsigned short, 3>", "haar512"): {"sha": "02be9c317bd1aa8b", "fetch_kib": 131115.0,
                                                   "write_kib": 344064.0, "fetch_factor": 1.9998,
                                                   "write_factor": 1.0},
-    ("k_attn_mfma<64, 3, false, false>", "grid64"): {"sha": "1e4d38cadd42d5de", "fetch_kib": 12554.1,
-                                                     "write_kib": 8192.0, "fetch_factor": 1.9998,
+    ("k_attn_mfma<64, 3, false, true>", "grid64"): {"sha": "a893af69af938bb2", "fetch_kib": 12662.0,
+                                                    "write_kib": 8456.2, "fetch_factor": 1.99985,
+                                                    "write_factor": 1.0},
+    ("k_attn_mfma<64, 3, false, false>", "grid64"): {"sha": "a893af69af938bb2", "fetch_kib": 12552.2,
+                                                     "write_kib": 8192.0, "fetch_factor": 1.99985,
                                                      "write_factor": 1.0},
 }
 
@@ -162,6 +168,12 @@ class Runner:
         self.out = torch.empty_like(self.q)
         self.out_dense = torch.empty_like(self.q)
 
+    def fused(self) -> bool:
+        """True when the step is the fused form (pooling launch + gated attention)."""
+        from paper_2605_15684_amd import _lib
+        return self.w.gate == "topk" and _lib.forward_kernel(self.desc, mode=2) != \
+            _lib.forward_kernel(self.desc, mode=0)
+
     def step(self):
         """One layer call: ssba_forward_topk (gate fused into attention) for
         the top-k gate; the static gates go through the two-call form."""
@@ -195,6 +207,15 @@ class Runner:
 
     def run_dense(self):
         self.ssba.forward_dense(self.q, self.k, self.v, self.desc, self.out_dense)
+
+    def run_pool(self):
+        """The step's pooling launch alone (ssba_pool_keys_ex)."""
+        self.ssba.pool_keys(self.k, self.desc, self.scratch)
+
+    def run_gated(self):
+        """The step's gated attention launch alone (ssba_forward_gated_ex), on
+        the pooled key sums the last step or run_pool left in the scratch."""
+        self.ssba.forward_gated(self.q, self.k, self.v, self.desc, self.index, self.scratch, self.out)
 
     def timed_steps(self, steps: int):
         """Whole steps (index + forward) back to back: wall ms and event ms per step."""
@@ -317,14 +338,20 @@ def measure(w, steps: int, warmup: int, dense_steps: int, graph: bool = True, se
     # in the sequence (the clock settles over the first milliseconds of load).
     for _ in range(3):
         r.run_dense()
-    spans = {"two": [], "idx": [], "fwd": [], "dense": []}
+    fused = r.fused()
+    spans = {"two": [], "idx": [], "fwd": [], "dense": [], "gated": [], "pool": []}
     for _ in range(REPEATS):
         spans["two"].append(r._span(r.step_two_calls, steps))
         spans["idx"].append(r._span(r.run_index, steps))
         spans["fwd"].append(r._span(r.run_fwd, steps))
         spans["dense"].append(r._span(r.run_dense, dense_steps))
+        if fused:
+            spans["pool"].append(r._span(r.run_pool, steps))
+            spans["gated"].append(r._span(r.run_gated, steps))
     two_ms, idx_ms, fwd_ms, dense_ms = (statistics.median(spans[key])
                                         for key in ("two", "idx", "fwd", "dense"))
+    gated_ms = statistics.median(spans["gated"]) if fused else None
+    pool_ms = statistics.median(spans["pool"]) if fused else None
     cold_step_ms = r.cold_ms(r.step)
     cold_fwd_ms = r.cold_ms(r.run_fwd)
     graph_ms = None
@@ -341,7 +368,8 @@ def measure(w, steps: int, warmup: int, dense_steps: int, graph: bool = True, se
     return r, {
         "ms_step_wall": wall_ms, "ms_step_eager": step_ms, "ms_step_graph": graph_ms,
         "ms_step": best_ms, "ms_step_two_calls": two_ms, "ms_index": idx_ms, "ms_fwd": fwd_ms,
-        "ms_dense": dense_ms, "ms_step_cold": cold_step_ms, "ms_fwd_cold": cold_fwd_ms, "gflop": f / 1e9, "gflop_dense": flops(w, dense=True) / 1e9,
+        "ms_dense": dense_ms, "ms_gated": gated_ms, "ms_pool": pool_ms, "ms_step_cold": cold_step_ms,
+        "ms_fwd_cold": cold_fwd_ms, "gflop": f / 1e9, "gflop_dense": flops(w, dense=True) / 1e9,
         "tflops_fwd": f / (fwd_ms * 1e-3) / 1e12,
         "tflops_step": f / (best_ms * 1e-3) / 1e12,
         "tflops_dense": flops(w, dense=True) / (dense_ms * 1e-3) / 1e12,
@@ -651,14 +679,19 @@ def main():
         return
     r, m = measure(w, args.steps, args.warmup, max(20, args.steps // 4), settle_ms=args.settle_ms)
     f = flops(w)
-    achieved = f / (m["ms_fwd"] * 1e-3) / 1e12
     from paper_2605_15684_amd import _lib
-    kernel = _lib.forward_kernel(r.desc, mode=0)
-    traffic = measured_traffic(kernel, w.name)
-    roofline = {"bound": "mfma", "kernel": kernel, "achieved": round(achieved, 2),
+
+    def roofline_of(kernel, ms):
+        achieved = f / (ms * 1e-3) / 1e12
+        traffic = measured_traffic(kernel, w.name)
+        return {"bound": "mfma", "kernel": kernel, "achieved": round(achieved, 2),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                 "traffic": None if traffic is None else round(traffic),
-                "traffic_unit": "HBM bytes/launch", "sources_sha": sources_sha(kernel)}
+                "traffic_unit": "HBM bytes/launch", "ms_per_launch": round(ms, 5),
+                "sources_sha": sources_sha(kernel)}
+
+    ungated = roofline_of(_lib.forward_kernel(r.desc, mode=0), m["ms_fwd"])
+    roofline = roofline_of(_lib.forward_kernel(r.desc, mode=2), m["ms_gated"]) if m["ms_gated"] else ungated
     mfma_meas = measured_mfma_tflops()
     cpu = None if args.no_cpu else cpu_baseline(r)
     line = {
@@ -671,6 +704,8 @@ def main():
         "config": {"workload": f"{w.name}: {describe(w)}", "global_batch": w.batch,
                    "seq_len": w.seq_len, "parallelism": "none (1 GPU)"},
         "ms_fwd": round(m["ms_fwd"], 5), "ms_index": round(m["ms_index"], 5),
+        "ms_gated": None if m["ms_gated"] is None else round(m["ms_gated"], 5),
+        "ms_pool": None if m["ms_pool"] is None else round(m["ms_pool"], 5),
         "ms_dense": round(m["ms_dense"], 5), "ms_step_wall": round(m["ms_step_wall"], 5),
         "ms_step_eager": round(m["ms_step_eager"], 5),
         "ms_step_two_calls": round(m["ms_step_two_calls"], 5),
@@ -683,7 +718,7 @@ def main():
         "speedup_vs_dense_kernel": round(m["speedup_kernel"], 3),
         "speedup_vs_dense_step": round(m["speedup_step"], 3),
         "gflop_computed": round(m["gflop"], 3), "gflop_dense": round(m["gflop_dense"], 3),
-        "roofline": roofline, "cpu_baseline": cpu,
+        "roofline": roofline, "roofline_ungated": ungated, "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
 

@@ -171,6 +171,27 @@ ssba_status ssba_forward_dense(const ssba_desc* d, const void* q, const void* k,
 ssba_status ssba_forward_topk(const ssba_desc* d, const void* q, const void* k, const void* v,
                               int32_t* index, void* scratch, void* o, void* hip_stream);
 
+/* The two launches of ssba_forward_topk's fused form, callable one at a time
+ * (Algorithm 1: ssba_pool_keys_ex is the pooling of K, Eq. 1;
+ * ssba_forward_gated_ex the affinity, ranking and attention steps).
+ * ssba_forward_topk_ex with the fused form is exactly ssba_pool_keys_ex then
+ * ssba_forward_gated_ex on one stream.  Both need d->gate == SSBA_GATE_TOPK,
+ * bf16, 8x8 blocks, head_dim 64 or 128 and at most 64 blocks, and return
+ * SSBA_ERR_UNSUPPORTED otherwise (ssba_forward_topk then runs the two calls).
+ * ssba_pool_keys_ex writes the pooled key sums of every (batch, head) into
+ * `scratch` (fp64, at the place the gated launch reads them); it reads only k.
+ * ssba_forward_gated_ex reads those sums, so `scratch` must hold what
+ * ssba_pool_keys_ex wrote for the same k and descriptor (anything else gives
+ * undefined index rows, never an out-of-bounds access: every id is range-
+ * checked); it writes index, the status flags in scratch and o, as
+ * ssba_forward_topk does.  Sizes, alignment and errors as for
+ * ssba_forward_topk_ex. */
+ssba_status ssba_pool_keys_ex(const ssba_desc* d, const void* k, void* scratch, size_t scratch_bytes,
+                              void* hip_stream);
+ssba_status ssba_forward_gated_ex(const ssba_desc* d, const void* q, const void* k, const void* v,
+                                  int32_t* index, size_t index_bytes, void* scratch, size_t scratch_bytes,
+                                  void* o, void* hip_stream);
+
 /* ssba_forward_topk with the sizes of `index` and `scratch` in bytes. */
 ssba_status ssba_forward_topk_ex(const ssba_desc* d, const void* q, const void* k, const void* v,
                                  int32_t* index, size_t index_bytes, void* scratch, size_t scratch_bytes,

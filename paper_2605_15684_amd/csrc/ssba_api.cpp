@@ -256,6 +256,23 @@ bool gated_supported(const ssba_desc* d, const Shape& s) {
          ssba::mfma_supported(d->head_dim, 8, false, s.n_tiles, s.seq, (int64_t)s.seq * s.st);
 }
 
+// Checks shared by the two launches of the fused top-k form; `attention`
+// for the gated attention launch (Q, V, O and the index too).
+ssba_status check_fused(const ssba_desc* d, Shape* s, const void* q, const void* k, const void* v,
+                        const int32_t* index, size_t index_bytes, const void* scratch, size_t scratch_bytes,
+                        const void* o, bool attention) {
+  ssba_status st = check_desc(d, s);
+  if (st != SSBA_OK) return st;
+  if (d->gate != SSBA_GATE_TOPK || !gated_supported(d, *s)) return SSBA_ERR_UNSUPPORTED;
+  if (!k || !scratch || !aligned(k, 16) || !aligned(scratch, 16)) return SSBA_ERR_ARG;
+  if (attention && (!q || !v || !o || !index || !aligned(q, 16) || !aligned(v, 16) || !aligned(o, 16) ||
+                    !aligned(index, 4)))
+    return SSBA_ERR_ARG;
+  if (scratch_bytes < scratch_bytes_of(d, *s) || (attention && index_bytes < index_bytes_of(d, *s)))
+    return SSBA_ERR_WORKSPACE;
+  return SSBA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -305,6 +322,35 @@ ssba_status ssba_forward_dense(const ssba_desc* d, const void* q, const void* k,
   return run_attention(d, q, k, v, nullptr, kUnchecked, o, stream, true);
 }
 
+ssba_status ssba_pool_keys_ex(const ssba_desc* d, const void* k, void* scratch, size_t scratch_bytes,
+                              void* stream) {
+  Shape s;
+  const ssba_status st = check_fused(d, &s, nullptr, k, nullptr, nullptr, 0, scratch, scratch_bytes, nullptr,
+                                     false);
+  if (st != SSBA_OK) return st;
+  const IndexArgs ia = index_args(d, s, nullptr, k, nullptr, scratch);
+  return ssba::launch_pool_keys(ia, static_cast<hipStream_t>(stream)) == hipSuccess ? SSBA_OK : SSBA_ERR_HIP;
+}
+
+ssba_status ssba_forward_gated_ex(const ssba_desc* d, const void* q, const void* k, const void* v,
+                                  int32_t* index, size_t index_bytes, void* scratch, size_t scratch_bytes,
+                                  void* o, void* stream) {
+  Shape s;
+  const ssba_status st = check_fused(d, &s, q, k, v, index, index_bytes, scratch, scratch_bytes, o, true);
+  if (st != SSBA_OK) return st;
+  // Each block's pooled query sum is formed in the kernel from its own Q
+  // rows; the pooled key sums come from ssba_pool_keys_ex.
+  const IndexArgs ia = index_args(d, s, q, k, index, scratch);
+  AttnArgs aa = attn_args(d, s, q, k, v, nullptr, o, false);
+  aa.gated = 1;
+  aa.keep = d->keep;
+  aa.kb = ia.kb;
+  aa.index_out = index;
+  aa.flags = ia.flags;
+  const hipError_t e = ssba::launch_attn_bf16(aa, d->head_dim, d->tile, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? SSBA_OK : SSBA_ERR_HIP;
+}
+
 ssba_status ssba_forward_topk_ex(const ssba_desc* d, const void* q, const void* k, const void* v,
                                  int32_t* index, size_t index_bytes, void* scratch, size_t scratch_bytes,
                                  void* o, void* stream) {
@@ -322,19 +368,9 @@ ssba_status ssba_forward_topk_ex(const ssba_desc* d, const void* q, const void* 
     st = ssba_build_index_ex(d, q, k, index, index_bytes, scratch, scratch_bytes, stream);
     return st != SSBA_OK ? st : ssba_forward_ex(d, q, k, v, index, index_bytes, o, stream);
   }
-  // Pooled key sums, then the attention kernel, which forms each block's
-  // pooled query sum from its own Q rows, gates the block and attends.
-  IndexArgs ia = index_args(d, s, q, k, index, scratch);
-  AttnArgs aa = attn_args(d, s, q, k, v, nullptr, o, false);
-  aa.gated = 1;
-  aa.keep = d->keep;
-  aa.kb = ia.kb;
-  aa.index_out = index;
-  aa.flags = ia.flags;
-  hipStream_t hs = static_cast<hipStream_t>(stream);
-  hipError_t e = ssba::launch_pool_keys(ia, hs);
-  if (e == hipSuccess) e = ssba::launch_attn_bf16(aa, d->head_dim, d->tile, hs);
-  return e == hipSuccess ? SSBA_OK : SSBA_ERR_HIP;
+  // Pooled key sums, then the attention kernel, which gates each block and attends.
+  st = ssba_pool_keys_ex(d, k, scratch, scratch_bytes, stream);
+  return st != SSBA_OK ? st : ssba_forward_gated_ex(d, q, k, v, index, index_bytes, scratch, scratch_bytes, o, stream);
 }
 
 ssba_status ssba_forward_topk(const ssba_desc* d, const void* q, const void* k, const void* v,

@@ -175,6 +175,30 @@ def forward_topk(q, k, v, desc, index=None, scratch=None, out=None):
     return index, scratch, out
 
 
+def pool_keys(k, desc, scratch):
+    """The pooling launch of the fused top-k form alone (ssba_pool_keys_ex):
+    writes the pooled key sums into `scratch` (from alloc_workspace)."""
+    if not (isinstance(k, torch.Tensor) and k.is_cuda and k.dtype == torch.bfloat16):
+        raise ValueError("k must be a bf16 GPU tensor laid out as desc says")
+    _check_buffer(scratch, "scratch")
+    _lib.check(_lib.pool_keys(desc, k.data_ptr(), scratch.data_ptr(), _stream(k.device), _nbytes(scratch)),
+               "ssba_pool_keys")
+    return scratch
+
+
+def forward_gated(q, k, v, desc, index, scratch, out):
+    """The gated attention launch of the fused top-k form alone
+    (ssba_forward_gated_ex): `scratch` must hold what pool_keys wrote for
+    this k.  pool_keys then forward_gated is exactly forward_topk."""
+    _check_tensors(desc, q, k, v, out)
+    _check_buffer(index, "index", torch.int32)
+    _check_buffer(scratch, "scratch")
+    _lib.check(_lib.forward_gated(desc, q.data_ptr(), k.data_ptr(), v.data_ptr(), index.data_ptr(),
+                                  scratch.data_ptr(), out.data_ptr(), _stream(q.device), _nbytes(index),
+                                  _nbytes(scratch)), "ssba_forward_gated")
+    return index, scratch, out
+
+
 def forward_layers(layers, desc, index=None, scratch=None):
     """A stack of SSBA layers in one call (ssba_forward_layers).
 

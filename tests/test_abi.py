@@ -324,3 +324,31 @@ def test_noalloc_rejects_scratch_beyond_its_array(lib):
     w = _desc(gate=_lib.GATE_WINDOW, win_h=2, win_w=2)
     assert _lib.forward_topk_noalloc(w, fake, fake, fake, fake, fake, None, 1 << 30) == _lib.SSBA_ERR_ARG
     assert lib.ssba_forward_topk_noalloc(None, fake, fake, fake, fake, 1 << 30, fake, None) == _lib.SSBA_ERR_ARG
+
+
+def test_split_fused_launches_checked_before_launch(lib):
+    """ssba_pool_keys_ex and ssba_forward_gated_ex (the two launches of the
+    fused top-k form) reject, before anything is launched, shapes the gated
+    kernel does not take (SSBA_ERR_UNSUPPORTED), missing or misaligned
+    buffers (SSBA_ERR_ARG) and short workspaces (SSBA_ERR_WORKSPACE)."""
+    fake = 0x100000
+    d = _desc()
+    ib, sb = _lib.workspace_size(d)
+    U, A, W = _lib.SSBA_ERR_UNSUPPORTED, _lib.SSBA_ERR_ARG, _lib.SSBA_ERR_WORKSPACE
+    for other in (_desc(tile=16), _desc(gate=_lib.GATE_TOPK_SHARED),
+                  _desc(dtype=_lib.DT_F32)):
+        assert _lib.pool_keys(other, fake, fake, None, 1 << 30) == U
+        assert _lib.forward_gated(other, fake, fake, fake, fake, fake, fake, None, 1 << 30, 1 << 30) == U
+    assert _lib.pool_keys(d, None, fake, None, sb) == A
+    assert _lib.pool_keys(d, fake, None, None, sb) == A
+    assert _lib.pool_keys(d, fake + 2, fake, None, sb) == A
+    assert _lib.pool_keys(d, fake, fake, None, sb - 1) == W
+    for i in range(6):   # q, k, v, index, scratch, o in turn missing
+        ptrs = [fake] * 6
+        ptrs[i] = None
+        assert _lib.forward_gated(d, *ptrs, None, ib, sb) == A
+    assert _lib.forward_gated(d, fake, fake, fake, fake, fake, fake + 8, None, ib, sb) == A
+    assert _lib.forward_gated(d, fake, fake, fake, fake, fake, fake, None, ib - 1, sb) == W
+    assert _lib.forward_gated(d, fake, fake, fake, fake, fake, fake, None, ib, sb - 1) == W
+    bad = _desc(keep=0)
+    assert _lib.pool_keys(bad, fake, fake, None, sb) == A

@@ -283,6 +283,26 @@ def test_forward_topk_equals_build_index_then_forward(w):
     assert torch.equal(out1, out2)
 
 
+@pytest.mark.parametrize("w", TOPK_CASES[:5], ids=_ids)
+def test_pool_keys_then_forward_gated_equals_forward_topk(w):
+    """The fused form's two launches called one at a time give the fused
+    call's index rows, status flags and output bit for bit; the index is the
+    oracle's."""
+    from paper_2605_15684_amd import ssba
+    (q, k, _), (qg, kg, vg) = inputs(w)
+    desc = gpu_desc(w, qg)
+    index1, scratch1, out1 = ssba.forward_topk(qg, kg, vg, desc)
+    index2, scratch2 = ssba.alloc_workspace(desc, qg.device)
+    index2.fill_(-5)
+    out2 = torch.full_like(out1, float("nan"))
+    ssba.pool_keys(kg, desc, scratch2)
+    ssba.forward_gated(qg, kg, vg, desc, index2, scratch2, out2)
+    torch.cuda.synchronize()
+    assert torch.equal(index1, index2) and torch.equal(out1, out2)
+    assert ssba.read_status(desc, scratch2) == 0
+    assert np.array_equal(index2.cpu().numpy(), oracle_index(w, q, k))
+
+
 def test_forward_topk_full_size_against_oracle():
     from paper_2605_15684_amd import ssba
     w = preset("grid64")
