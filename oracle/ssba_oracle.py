@@ -332,7 +332,7 @@ def transpose_index(index: np.ndarray) -> np.ndarray:
 
 
 def attention_backward(q, k, v, dout, index, *, grid_h, grid_w, tile, shift=(0, 0), n_text=0,
-                       scale=None, heads=None):
+                       scale=None, heads=None, row_chunk=None):
     """Gradients of the SSBA attention output with respect to Q, K and V, fp64.
 
     With P = softmax(scale Q K^T + mask) over the token mask of the index
@@ -341,6 +341,10 @@ def attention_backward(q, k, v, dout, index, *, grid_h, grid_w, tile, shift=(0, 
       dQ = scale dS K,  dK = scale dS^T Q;
     also the natural-log log-sum-exp of each row's masked scaled logits.
     Returns (dq, dk, dv, lse); pairs outside ``heads`` are left NaN.
+
+    ``row_chunk`` bounds memory at large T: the query rows are taken that
+    many at a time (P, dP and dS of a row need only that row), and their
+    terms of dV and dK are added up over the chunks.
     """
     b_n, h_n, t, c = q.shape
     if scale is None or scale <= 0:
@@ -350,20 +354,26 @@ def attention_backward(q, k, v, dout, index, *, grid_h, grid_w, tile, shift=(0, 
     dv = np.full(q.shape, np.nan)
     lse = np.full((b_n, h_n, t), np.nan)
     pairs = [(b, h) for b in range(b_n) for h in range(h_n)] if heads is None else list(heads)
-    rows = np.arange(t)
+    step = t if not row_chunk else int(row_chunk)
     for b, h in pairs:
         qq, kk, vv, gg = (np.asarray(x[b, h], np.float64) for x in (q, k, v, dout))
-        mask = token_mask_rows(index[b, h], rows, grid_h=grid_h, grid_w=grid_w, tile=tile,
-                               shift=shift, n_text=n_text)
-        logits = np.where(mask, scale * (qq @ kk.T), -np.inf)
-        m = logits.max(axis=-1, keepdims=True)
-        e = np.exp(logits - m)
-        s = e.sum(axis=-1, keepdims=True)
-        p = e / s
-        lse[b, h] = (m + np.log(s))[:, 0]
-        dp = gg @ vv.T
-        ds = p * (dp - np.sum(p * dp, axis=-1, keepdims=True))
-        dv[b, h] = p.T @ gg
-        dq[b, h] = scale * (ds @ kk)
-        dk[b, h] = scale * (ds.T @ qq)
+        dk_bh = np.zeros((t, c))
+        dv_bh = np.zeros((t, c))
+        for r0 in range(0, t, step):
+            rows = np.arange(r0, min(r0 + step, t))
+            mask = token_mask_rows(index[b, h], rows, grid_h=grid_h, grid_w=grid_w, tile=tile,
+                                   shift=shift, n_text=n_text)
+            logits = np.where(mask, scale * (qq[rows] @ kk.T), -np.inf)
+            m = logits.max(axis=-1, keepdims=True)
+            e = np.exp(logits - m)
+            s = e.sum(axis=-1, keepdims=True)
+            p = e / s
+            lse[b, h, rows] = (m + np.log(s))[:, 0]
+            dp = gg[rows] @ vv.T
+            ds = p * (dp - np.sum(p * dp, axis=-1, keepdims=True))
+            dv_bh += p.T @ gg[rows]
+            dq[b, h, rows] = scale * (ds @ kk)
+            dk_bh += scale * (ds.T @ qq[rows])
+        dk[b, h] = dk_bh
+        dv[b, h] = dv_bh
     return dq, dk, dv, lse
