@@ -618,7 +618,8 @@ def measure_backward(w, steps: int, warmup: int) -> dict:
     f_bwd = 2.5 * f_fwd
     tf_bwd = f_bwd / (ms_bwd * 1e-3) / 1e12
     return {
-        "metric": "SSBA backward TFLOP/s (gradients of the attend step, 4096 tokens, 84% sparse)",
+        "metric": f"SSBA backward TFLOP/s (gradients of the attend step, {w.seq_len} tokens, "
+                  f"{100 * (1 - pairs_per_bh(w) / w.seq_len ** 2):.0f}% sparse)",
         "value": round(tf_bwd, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
         "ms_per_step": round(ms_bwd, 5), "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"{w.name}: {describe(w)}"},

@@ -227,8 +227,8 @@ ssba_status ssba_backward_workspace_size(const ssba_desc* d, size_t* scratch_byt
  * queries see their kept blocks and the text keys, text queries see every
  * key.  All tensors bf16 with the descriptor's layout (dq, dk, dv written in
  * full, every row); products on MFMA with fp32 accumulation, P and dS rounded
- * to bf16 before their products.  bf16, 8x8 blocks, head_dim 64 or 128, at
- * most 64 blocks; other shapes return SSBA_ERR_UNSUPPORTED.  The gate fields
+ * to bf16 before their products.  bf16, 8x8 or 16x16 blocks, head_dim 64 or
+ * 128, at most 64 blocks; other shapes return SSBA_ERR_UNSUPPORTED.  The gate fields
  * of the descriptor are not used. */
 ssba_status ssba_backward(const ssba_desc* d, const void* q, const void* k, const void* v, const void* o,
                           const void* dout, const float* lse, const int32_t* index, void* dq, void* dk,

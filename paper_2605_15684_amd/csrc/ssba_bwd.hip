@@ -5,14 +5,19 @@
 //   dQ = scale dS K,  dK = scale dS^T Q,
 // with P recomputed from the forward's per-row log-sum-exp.
 //
-// Kernels (bf16 tensors, 8x8 blocks, head_dim 64 / 128, at most 64 blocks):
+// Kernels (bf16 tensors, 8x8 or 16x16 blocks, head_dim 64 / 128, at most 64
+// blocks).  Work goes in chunks of 64 rows: an 8x8 block, or a quarter (four
+// block rows) of a 16x16 block; an image chunk is named by block * GPB +
+// quarter (GPB = chunks per block), a text chunk t by -1 - t.
 //   k_bwd_dq        query side, like the forward: a 64-query group forms D and
 //                   the log-sum-exp in log2 units of its rows and the 64-bit
 //                   mask of its kept blocks (all stored for the key side),
-//                   then walks its kept key blocks and the text keys;
+//                   then walks the chunks of its kept key blocks and the text
+//                   keys;
 //   k_bwd_dkdv      key side: a 64-key group reads the head's masks, ballots
-//                   the query blocks that kept it (ascending) and walks them
-//                   plus the text queries (text key groups: every query).
+//                   the query blocks that kept its block (ascending) and walks
+//                   their chunks plus the text queries (text key groups:
+//                   every query).
 // Both main kernels use v_mfma_f32_32x32x16_bf16 with four waves per group:
 // two row halves of the group x two streams over each 64-row chunk of the
 // other side, merged once at the end.  Chunks are copied into LDS with
@@ -107,13 +112,15 @@ __device__ __forceinline__ float swap_sum(float v) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// Sequence row of row s (0..63) of chunk `src`: an image block (src >= 0) of
-// the shifted frame, or text chunk -1 - src (rows 64 c ..), clamped into the
-// text rows; `valid` is false for clamped rows.
+// Sequence row of row s (0..63) of chunk `src`: image chunk src = block * GPB
+// + quarter of the shifted frame (GPB = 1 << QL chunks per block), or text
+// chunk -1 - src (rows 64 c ..), clamped into the text rows; `valid` is false
+// for clamped rows.
+template <int QL>
 __device__ __forceinline__ int chunk_row(const Frame& f, int src, int s, bool& valid) {
   if (src >= 0) {
     valid = true;
-    return frame_row(f, src, s);
+    return frame_row(f, src >> QL, 64 * (src & ((1 << QL) - 1)) + s);
   }
   const int r = 64 * (-1 - src) + s;
   valid = r < f.n_text;
@@ -137,26 +144,30 @@ __device__ __forceinline__ void swizzle_offsets(int sub, int lane, unsigned (&zo
 }
 
 // Byte offsets, inside the (batch, head) slice, of this wave's copy
-// instructions for half `hf` of chunk `src` (an image block of 8x8 tokens,
-// or text chunk -1 - src with rows past the text clamped to its last row).
-// The block origin is found once per chunk; an instruction's rows lie in one
-// block row (KPI <= 8), so only the column depends on the lane.
-template <int D>
+// instructions for half `hf` of chunk `src` (image chunk block * GPB +
+// quarter of a 2^TL x 2^TL block, or text chunk -1 - src with rows past the
+// text clamped to its last row).  The block origin is found once per chunk;
+// an instruction's rows lie in one block row (KPI <= 2^TL), so only the
+// column depends on the lane.
+template <int D, int TL>
 __device__ __forceinline__ void copy_offsets(const Frame& f, int src, int hf, int sub, unsigned st2,
                                              const unsigned (&zoff)[BShape<D>::NIW], int lane,
                                              unsigned (&off)[BShape<D>::NIW]) {
   using S = BShape<D>;
-  static_assert(S::KPI <= 8 && 8 % S::KPI == 0, "an instruction stays inside one block row");
+  constexpr int TILE = 1 << TL, QL = 2 * TL - 6;
+  static_assert(S::KPI <= TILE && TILE % S::KPI == 0, "an instruction stays inside one block row");
   const int kin = lane / S::CPR;
   if (src >= 0) {
-    const int ty = src / f.nx, tx = src - ty * f.nx;
-    const int y0 = (ty << 3) - f.sy + 4 * hf, x0 = (tx << 3) - f.sx;
+    const int blk = src >> QL, quarter = src & ((1 << QL) - 1);
+    const int ty = blk / f.nx, tx = blk - ty * f.nx;
+    const int y0 = (ty << TL) - f.sy, x0 = (tx << TL) - f.sx;
 #pragma unroll
     for (int mm = 0; mm < S::NIW; ++mm) {
-      const int k = S::KPI * (S::NIW * sub + mm);   // first row of the instruction
-      int y = y0 + (k >> 3);
+      // first slot of the instruction in the block
+      const int slot = 64 * quarter + 32 * hf + S::KPI * (S::NIW * sub + mm);
+      int y = y0 + (slot >> TL);
       y += y < 0 ? f.grid_h : 0;
-      int x = x0 + (k & 7) + kin;
+      int x = x0 + (slot & (TILE - 1)) + kin;
       x += x < 0 ? f.grid_w : 0;
       off[mm] = st2 * (unsigned)(f.n_text + y * f.grid_w) + st2 * (unsigned)x + zoff[mm];
     }
@@ -181,18 +192,22 @@ __device__ __forceinline__ void copy_half(const __amdgpu_buffer_rsrc_t& rs, cons
 }
 
 // One float per chunk row (the log-sum-exp or D of the 64 rows) into LDS.
+template <int QL>
 __device__ __forceinline__ void copy_rowvals(const __amdgpu_buffer_rsrc_t& rs, const Frame& f, int src,
                                              float* dst, int lane) {
   bool valid;
-  const int row = chunk_row(f, src, lane, valid);
+  const int row = chunk_row<QL>(f, src, lane, valid);
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)dst, 4, 4u * (unsigned)row, 0, 0, 0);
 }
 
 // Workgroup -> (b, h, group): every (b, h) owns n_text_groups text groups and
-// n_tiles image groups; with a head count divisible by 8 each XCD (hardware
-// ids go round-robin over the 8) gets whole heads, text groups first.
+// n_tiles << QL image groups (one per chunk of every block); with a head count
+// divisible by 8 each XCD (hardware ids go round-robin over the 8) gets whole
+// heads, text groups first.
+template <int QL>
 __device__ __forceinline__ void group_of(const BwdArgs& a, int& bh, int& r) {
-  const int bid = blockIdx.x, nbh = a.batch * a.heads, gpb = a.n_text_groups + a.n_tiles;
+  const int n_img = a.n_tiles << QL;
+  const int bid = blockIdx.x, nbh = a.batch * a.heads, gpb = a.n_text_groups + n_img;
   if ((nbh & 7) == 0) {
     const int xcd = bid & 7, s = bid >> 3, hpx = nbh >> 3;
     const int nt = a.n_text_groups;
@@ -201,8 +216,8 @@ __device__ __forceinline__ void group_of(const BwdArgs& a, int& bh, int& r) {
       r = s % nt;
     } else {
       const int s2 = s - hpx * nt;
-      bh = xcd * hpx + s2 / a.n_tiles;
-      r = nt + s2 % a.n_tiles;
+      bh = xcd * hpx + s2 / n_img;
+      r = nt + s2 % n_img;
     }
   } else {
     bh = bid / gpb;
@@ -217,10 +232,11 @@ __device__ __forceinline__ void group_of(const BwdArgs& a, int& bh, int& r) {
 // the forward), P^T = exp2(S^T), dP^T = V dO^T, dS^T = P^T (dP^T - D),
 // dQ^T += K^T dS^T.
 // --------------------------------------------------------------------------
-template <int D>
+template <int D, int TL>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k_bwd_dq(BwdArgs a) {
   using S = BShape<D>;
   constexpr int HALF = S::HALF, NKS = S::NKS, NDB = S::NDB;
+  constexpr int QL = 2 * TL - 6, GPB = 1 << QL;   // chunks (64-row groups) per block
   // K and V buffers A and B (alternate chunks; stream s at byte HALF s).
   // Separate variables, each named statically by every access, so that the
   // compiler can tell a read of one chunk from the copy of the next in flight.
@@ -229,7 +245,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
   __shared__ __attribute__((aligned(16))) char vA[2 * HALF];
   __shared__ __attribute__((aligned(16))) char vB[2 * HALF];
   int bh, r;
-  group_of(a, bh, r);
+  group_of<QL>(a, bh, r);
   const int b = bh / a.heads, h = bh - b * a.heads;
   const int64_t off = (int64_t)b * a.sb + (int64_t)h * a.sh;
   const u16* qbase = static_cast<const u16*>(a.q) + off;
@@ -241,29 +257,33 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int qh = w & 1, sk = w >> 1, hw = lane >> 5, l32 = lane & 31;
 
-  // This lane's query row and the chunk plan.
+  // This lane's query row and the chunk plan.  An image group is chunk gq of
+  // query block qi.
   const bool text_group = r < a.n_text_groups;
+  const int g = r - a.n_text_groups, qi = g >> QL, gq = g & (GPB - 1);
   int qrow;
   if (text_group) {
     const int q = 64 * r + 32 * qh + l32;
     qrow = q < a.f.n_text ? q : -1;
   } else {
-    qrow = frame_row(a.f, r - a.n_text_groups, 32 * qh + l32);
+    qrow = frame_row(a.f, qi, 64 * gq + 32 * qh + l32);
   }
   const int qr = max(qrow, 0);
   // Chunks: text groups see every key (the text chunks, then every image
-  // block in block order); image groups their kept blocks, then the text.
+  // chunk in block order); image groups the chunks of their kept blocks,
+  // then the text.
   const int n_txt = (a.f.n_text + 63) / 64;
   int n_img, listv = -1;
   if (text_group) {
-    n_img = a.n_tiles;
+    n_img = a.n_tiles << QL;
   } else {
-    const int32_t* list = a.index + ((int64_t)bh * a.n_tiles + (r - a.n_text_groups)) * (a.n_tiles + 1);
+    const int32_t* list = a.index + ((int64_t)bh * a.n_tiles + qi) * (a.n_tiles + 1);
     const int raw = list[0];
     const int ent = lane < a.n_tiles ? list[1 + lane] : 0;
-    n_img = min(max(raw, 0), a.n_tiles);
-    listv = lane < n_img ? ent : -1;
+    const int n_blk = min(max(raw, 0), a.n_tiles);
+    listv = lane < n_blk ? ent : -1;
     if ((unsigned)listv >= (unsigned)a.n_tiles) listv = -1;
+    n_img = n_blk << QL;
   }
   const int n = n_img + n_txt;
   // The kept blocks of an image group as a 64-bit mask, for the key side.
@@ -271,13 +291,13 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
   if (threadIdx.x == 0) kept_mask = 0ull;
   __syncthreads();
   if (!text_group && w == 0 && listv >= 0) atomicOr(&kept_mask, 1ull << listv);
-  // Chunk c -> source: image blocks first (block id, -1000000 marks an
-  // invalid id), then text chunk -1 - t.
+  // Chunk c -> source: image chunks first (block id * GPB + quarter;
+  // -1000000 marks an invalid id), then text chunk -1 - t.
   auto src_of = [&](int c) {
     if (c < n_img) {
       if (text_group) return c;
-      const int j = __builtin_amdgcn_readlane(listv, c);
-      return j >= 0 ? j : -1000000;   // invalid id: masked (rows clamped to text row 0 / block 0)
+      const int j = __builtin_amdgcn_readlane(listv, c >> QL);
+      return j >= 0 ? (j << QL) + (c & (GPB - 1)) : -1000000;   // invalid id: masked (rows of chunk 0)
     }
     return -1 - (c - n_img);
   };
@@ -331,7 +351,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
   auto issue = [&](int c, char* kd, char* vd) {
     const int src = src_of(c);
     unsigned offs[S::NIW];
-    copy_offsets<D>(a.f, src == -1000000 ? 0 : src, sk, qh, 2u * (unsigned)st, zoff, lane, offs);
+    copy_offsets<D, TL>(a.f, src == -1000000 ? 0 : src, sk, qh, 2u * (unsigned)st, zoff, lane, offs);
     copy_half<D>(rk, offs, qh, kd + HALF * sk);
     copy_half<D>(rv, offs, qh, vd + HALF * sk);
   };
@@ -343,7 +363,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
   if (n > 0) issue(0, kA, vA);
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   __syncthreads();
-  if (!text_group && threadIdx.x == 0) a.kmask[(int64_t)bh * a.n_tiles + (r - a.n_text_groups)] = kept_mask;
+  if (!text_group && gq == 0 && threadIdx.x == 0) a.kmask[(int64_t)bh * a.n_tiles + qi] = kept_mask;
   // Chunk c from (kc, vc) while chunk c + 1 is copied into (kn, vn).
   auto body = [&](int c, const char* kc, const char* vc, char* kn, char* vn) {
     if (c + 1 < n) issue(c + 1, kn, vn);
@@ -428,10 +448,11 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
 // Per chunk: S = Q K^T (rows = queries), P = exp2(S scale log2 e - lse2),
 // dV^T += dO^T P, dP = dO V^T, dS = P (dP - D), dK^T += Q^T dS.
 // --------------------------------------------------------------------------
-template <int D>
+template <int D, int TL>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 64 ? 2 : 1))) k_bwd_dkdv(BwdArgs a) {
   using S = BShape<D>;
   constexpr int HALF = S::HALF, NKS = S::NKS, NDB = S::NDB;
+  constexpr int QL = 2 * TL - 6, GPB = 1 << QL;   // chunks (64-row groups) per block
   // Q, dO, lse2 and D buffers A and B (alternate chunks; query stream s of
   // Q / dO at byte HALF s), separate variables as in k_bwd_dq.
   __shared__ __attribute__((aligned(16))) char qA[2 * HALF];
@@ -443,7 +464,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
   __shared__ __attribute__((aligned(16))) float dA[64];   // D of the chunk's rows
   __shared__ __attribute__((aligned(16))) float dB[64];
   int bh, r;
-  group_of(a, bh, r);
+  group_of<QL>(a, bh, r);
   const int b = bh / a.heads, h = bh - b * a.heads;
   const int64_t off = (int64_t)b * a.sb + (int64_t)h * a.sh;
   const u16* qbase = static_cast<const u16*>(a.q) + off;
@@ -455,45 +476,44 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int kh = w & 1, qs = w >> 1, hw = lane >> 5, l32 = lane & 31;
 
-  // This lane's key row.
+  // This lane's key row.  An image group is chunk kq of key block kj.
   const bool text_group = r < a.n_text_groups;
+  const int g = r - a.n_text_groups, kj = g >> QL, kq = g & (GPB - 1);
   int krow;
   if (text_group) {
     const int kk = 64 * r + 32 * kh + l32;
     krow = kk < a.f.n_text ? kk : -1;
   } else {
-    krow = frame_row(a.f, r - a.n_text_groups, 32 * kh + l32);
+    krow = frame_row(a.f, kj, 64 * kq + 32 * kh + l32);
   }
   const int kr = max(krow, 0);
-  // Query chunks: the query blocks that kept this key block (text key
-  // groups: every block), then the text query chunks.
+  // Query chunks: the chunks of the query blocks that kept this key block
+  // (text key groups: every block), then the text query chunks.
   const int n_txt = (a.f.n_text + 63) / 64;
   int n_img;
   uint64_t members = 0;   // bit i: query block i kept this key block
   if (text_group) {
-    n_img = a.n_tiles;
+    n_img = a.n_tiles << QL;
   } else {
-    const int j = r - a.n_text_groups;
     const uint64_t m = lane < a.n_tiles ? a.kmask[(int64_t)bh * a.n_tiles + lane] : 0ull;
-    members = __ballot(((m >> j) & 1ull) != 0ull);
-    n_img = __popcll(members);
+    members = __ballot(((m >> kj) & 1ull) != 0ull);
+    n_img = __popcll(members) << QL;
   }
   const int n = n_img + n_txt;
-  // Sources in chunk order: the member query blocks ascending (text key
-  // groups: every block), then text chunk -1 - t.  Taken once each, when the
-  // chunk's copy is issued.
+  // Sources in chunk order: the chunks of the member query blocks ascending
+  // (text key groups: every chunk), then text chunk -1 - t.  Taken once
+  // each, when the chunk's copy is issued.
   uint64_t rest = members;
-  int next_blk = 0, next_txt = 0;
+  int next_img = 0, next_txt = 0, cur = 0;
   auto pop_src = [&]() {
-    if (text_group ? next_blk < a.n_tiles : rest != 0ull) {
-      int s2;
-      if (text_group) {
-        s2 = next_blk++;
-      } else {
-        s2 = (int)__builtin_ctzll(rest);
+    if (next_img < n_img) {
+      const int qc = next_img++ & (GPB - 1);
+      if (text_group) return (next_img - 1);
+      if (qc == 0) {   // next member block
+        cur = (int)__builtin_ctzll(rest);
         rest &= rest - 1ull;
       }
-      return s2;
+      return (cur << QL) + qc;
     }
     return -1 - next_txt++;
   };
@@ -520,11 +540,11 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
   swizzle_offsets<D>(kh, lane, zoff);
   auto issue = [&](int src, char* qd, char* gd, float* ld, float* dd) {
     unsigned offs[S::NIW];
-    copy_offsets<D>(a.f, src, qs, kh, 2u * (unsigned)st, zoff, lane, offs);
+    copy_offsets<D, TL>(a.f, src, qs, kh, 2u * (unsigned)st, zoff, lane, offs);
     copy_half<D>(rq, offs, kh, qd + HALF * qs);
     copy_half<D>(rg, offs, kh, gd + HALF * qs);
-    if (w == 0) copy_rowvals(rl, a.f, src, ld, lane);
-    if (w == 1) copy_rowvals(rdl, a.f, src, dd, lane);
+    if (w == 0) copy_rowvals<QL>(rl, a.f, src, ld, lane);
+    if (w == 1) copy_rowvals<QL>(rdl, a.f, src, dd, lane);
   };
 
   floatx16 dk[NDB], dv[NDB];
@@ -644,14 +664,23 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
 hipError_t launch_backward(const BwdArgs& a0, int head_dim, hipStream_t s) {
   BwdArgs a = a0;
   a.n_text_groups = (a.f.n_text + 63) / 64;
+  const int tl = a.f.tile_log2;
+  if ((head_dim != 64 && head_dim != 128) || (tl != 3 && tl != 4)) return hipErrorInvalidValue;
   const dim3 blk(256);
-  const dim3 grid((unsigned)(a.batch * a.heads * (a.n_text_groups + a.n_tiles)));
-  if (head_dim == 64) {
-    hipLaunchKernelGGL(k_bwd_dq<64>, grid, blk, 0, s, a);
-    hipLaunchKernelGGL(k_bwd_dkdv<64>, grid, blk, 0, s, a);
+  const int gpb = 1 << (2 * tl - 6);
+  const dim3 grid((unsigned)(a.batch * a.heads * (a.n_text_groups + a.n_tiles * gpb)));
+  if (head_dim == 64 && tl == 3) {
+    hipLaunchKernelGGL((k_bwd_dq<64, 3>), grid, blk, 0, s, a);
+    hipLaunchKernelGGL((k_bwd_dkdv<64, 3>), grid, blk, 0, s, a);
+  } else if (head_dim == 64) {
+    hipLaunchKernelGGL((k_bwd_dq<64, 4>), grid, blk, 0, s, a);
+    hipLaunchKernelGGL((k_bwd_dkdv<64, 4>), grid, blk, 0, s, a);
+  } else if (tl == 3) {
+    hipLaunchKernelGGL((k_bwd_dq<128, 3>), grid, blk, 0, s, a);
+    hipLaunchKernelGGL((k_bwd_dkdv<128, 3>), grid, blk, 0, s, a);
   } else {
-    hipLaunchKernelGGL(k_bwd_dq<128>, grid, blk, 0, s, a);
-    hipLaunchKernelGGL(k_bwd_dkdv<128>, grid, blk, 0, s, a);
+    hipLaunchKernelGGL((k_bwd_dq<128, 4>), grid, blk, 0, s, a);
+    hipLaunchKernelGGL((k_bwd_dkdv<128, 4>), grid, blk, 0, s, a);
   }
   return hipGetLastError();
 }

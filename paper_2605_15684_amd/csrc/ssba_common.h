@@ -150,7 +150,7 @@ hipError_t launch_attn_f32(const AttnArgs& a, int head_dim, int tile, hipStream_
 bool mfma_supported(int head_dim, int tile, bool dense, int n_tiles, int seq, int64_t span);
 hipError_t launch_attn_mfma(const AttnArgs& a, int head_dim, int tile, hipStream_t s);
 const char* mfma_kernel_name(int head_dim, int tile, bool dense, bool gated);
-// Backward: bf16, 8x8 blocks, head_dim 64 / 128, at most 64 blocks.
+// Backward: bf16, 8x8 or 16x16 blocks, head_dim 64 / 128, at most 64 blocks.
 bool bwd_supported(int head_dim, int tile, int n_tiles, int dtype);
 hipError_t launch_backward(const BwdArgs& a, int head_dim, hipStream_t s);
 // Name of the kernel launch_attn_bf16 / launch_attn_f32 would run.

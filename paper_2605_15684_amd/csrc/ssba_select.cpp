@@ -40,7 +40,8 @@ const char* attn_kernel_name(const AttnArgs& a, int head_dim, int tile, int dtyp
 }
 
 bool bwd_supported(int head_dim, int tile, int n_tiles, int dtype) {
-  return dtype == SSBA_DT_BF16 && (head_dim == 64 || head_dim == 128) && tile == 8 && n_tiles <= 64;
+  return dtype == SSBA_DT_BF16 && (head_dim == 64 || head_dim == 128) && (tile == 8 || tile == 16) &&
+         n_tiles <= 64;
 }
 
 }  // namespace ssba

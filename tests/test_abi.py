@@ -240,7 +240,8 @@ def test_haar_kernel_names(lib):
     assert _lib.haar_kernel_name(_hdesc(levels=1, dtype=_lib.DT_F32), True) == "k_haar_iwt<float, 1>"
 
 
-@pytest.mark.parametrize("kw", [{"tile": 16, "grid_h": 128, "grid_w": 128, "keep": 7},
+@pytest.mark.parametrize("kw", [{"tile": 16, "grid_h": 256, "grid_w": 256, "keep": 7},   # 256 blocks
+                                {"tile": 4, "grid_h": 32, "grid_w": 32, "keep": 4},
                                 {"dtype": _lib.DT_F32, "tile": 4, "grid_h": 16, "grid_w": 16, "keep": 4},
                                 {"grid_h": 128, "grid_w": 128}])      # 256 blocks
 def test_backward_unsupported_shapes_rejected_before_launch(lib, kw):
