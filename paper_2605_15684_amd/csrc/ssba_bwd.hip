@@ -156,7 +156,12 @@ __device__ __forceinline__ void copy_offsets(const Frame& f, int src, int hf, in
   using S = BShape<D>;
   constexpr int TILE = 1 << TL, QL = 2 * TL - 6;
   static_assert(S::KPI <= TILE && TILE % S::KPI == 0, "an instruction stays inside one block row");
-  const int kin = lane / S::CPR;
+  // The lane's row in an instruction, recomputed here from the lane id (two
+  // VALU instructions) rather than kept live across the chunk loop.
+  int ln = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+  asm volatile("" : "+v"(ln));
+  const int kin = ln / S::CPR;
+  (void)lane;
   if (src >= 0) {
     const int blk = src >> QL, quarter = src & ((1 << QL) - 1);
     const int ty = blk / f.nx, tx = blk - ty * f.nx;
@@ -233,7 +238,7 @@ __device__ __forceinline__ void group_of(const BwdArgs& a, int& bh, int& r) {
 // dQ^T += K^T dS^T.
 // --------------------------------------------------------------------------
 template <int D, int TL>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k_bwd_dq(BwdArgs a) {
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 64 ? 4 : 2))) k_bwd_dq(BwdArgs a) {
   using S = BShape<D>;
   constexpr int HALF = S::HALF, NKS = S::NKS, NDB = S::NDB;
   constexpr int QL = 2 * TL - 6, GPB = 1 << QL;   // chunks (64-row groups) per block
@@ -286,11 +291,6 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
     n_img = n_blk << QL;
   }
   const int n = n_img + n_txt;
-  // The kept blocks of an image group as a 64-bit mask, for the key side.
-  __shared__ unsigned long long kept_mask;
-  if (threadIdx.x == 0) kept_mask = 0ull;
-  __syncthreads();
-  if (!text_group && w == 0 && listv >= 0) atomicOr(&kept_mask, 1ull << listv);
   // Chunk c -> source: image chunks first (block id * GPB + quarter;
   // -1000000 marks an invalid id), then text chunk -1 - t.
   auto src_of = [&](int c) {
@@ -336,9 +336,19 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
     a.delta[rowid] = dlt;
     a.lse2[rowid] = lse2;
   }
-  floatx16 negl;
+  // dO fragments are read from LDS per chunk rather than held in registers
+  // (four waves per SIMD at D 64 need <= 128 VGPRs): fragment ks of query
+  // half qh at gstage + 1024 (NKS qh + ks), lane l's 16 bytes at 16 l, so the
+  // reads are linear.  Written by the stream-0 waves, read after the first
+  // barrier.
+  __shared__ __attribute__((aligned(16))) char gstage[2 * NKS * 1024];
+  if (sk == 0) {
 #pragma unroll
-  for (int e = 0; e < 16; ++e) negl[e] = -lse2;
+    for (int ks = 0; ks < NKS; ++ks)
+      *reinterpret_cast<bf16x8*>(gstage + 1024 * (NKS * qh + ks) + 16 * lane) = gf[ks];
+  }
+  const char* gfr = gstage + 1024 * NKS * qh + 16 * lane;
+  const float nlse = -lse2, ndlt = -dlt;
 
   const unsigned slice_bytes = 2u * (unsigned)((a.seq - 1) * st + D);
   const __amdgpu_buffer_rsrc_t rk =
@@ -363,7 +373,16 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
   if (n > 0) issue(0, kA, vA);
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   __syncthreads();
-  if (!text_group && gq == 0 && threadIdx.x == 0) a.kmask[(int64_t)bh * a.n_tiles + qi] = kept_mask;
+  // The kept blocks of an image block as a 64-bit mask, for the key side
+  // (stored by the block's first group; the ids are wave-uniform reads).
+  if (!text_group && gq == 0 && w == 0) {
+    uint64_t kept = 0ull;
+    for (int e = 0; e < (n_img >> QL); ++e) {
+      const int j = __builtin_amdgcn_readlane(listv, e);
+      if (j >= 0) kept |= 1ull << j;
+    }
+    if (lane == 0) a.kmask[(int64_t)bh * a.n_tiles + qi] = kept;
+  }
   // Chunk c from (kc, vc) while chunk c + 1 is copied into (kn, vn).
   auto body = [&](int c, const char* kc, const char* vc, char* kn, char* vn) {
     if (c + 1 < n) issue(c + 1, kn, vn);
@@ -378,11 +397,22 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
       const int base = 64 * (-1 - src) + 32 * sk;
       hi = min(max(a.f.n_text - base, 0), 32);
     }
-    floatx16 sc = negl, dp = floatx16{};
+    // The score accumulator starts from -lse2 and dP's from -D (so the
+    // products leave exp2's argument and dP - D); the splats are rebuilt per
+    // chunk from one register each instead of being held across the loop.
+    float nl = nlse, nd = ndlt;
+    asm volatile("" : "+v"(nl), "+v"(nd));
+    floatx16 sc, dp;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      sc[e] = nl;
+      dp[e] = nd;
+    }
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
       sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<D>(kt, lane, ks), qf[ks], sc, 0, 0, 0);
-      dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<D>(vt, lane, ks), gf[ks], dp, 0, 0, 0);
+      dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<D>(vt, lane, ks),
+                                                  *reinterpret_cast<const bf16x8*>(gfr + 1024 * ks), dp, 0, 0, 0);
     }
     if (lo > 0 || hi < 32) {   // rare: text tail or an invalid block id
       int l4 = lo - 4 * hw, h4 = hi - 4 * hw;
@@ -398,7 +428,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
     for (int rr = 0; rr < 16; rr += 2) {
       float ds[2];
 #pragma unroll
-      for (int u = 0; u < 2; ++u) ds[u] = __builtin_amdgcn_exp2f(sc[rr + u]) * (dp[rr + u] - dlt);
+      for (int u = 0; u < 2; ++u) ds[u] = __builtin_amdgcn_exp2f(sc[rr + u]) * dp[rr + u];
       pk[rr >> 1] = pack2(ds[0], ds[1]);
     }
 #pragma unroll
@@ -445,24 +475,37 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
 // --------------------------------------------------------------------------
 // dK, dV: one workgroup per 64-key group.  Wave w: key half kh = w % 2, query
 // stream qs = w / 2 (queries 32 qs .. 32 qs + 31 of every 64-query chunk).
-// Per chunk: S = Q K^T (rows = queries), P = exp2(S scale log2 e - lse2),
-// dV^T += dO^T P, dP = dO V^T, dS = P (dP - D), dK^T += Q^T dS.
+// Per chunk: S' = Q K'^T - lse2 (rows = queries; K' = K scale log2 e rounded
+// to bf16), P = exp2(S'), dV^T += dO^T P, dP - D = dO V^T - D, dS = P (dP - D),
+// dK^T += Q^T dS.  The two accumulators start from -lse2 and -D (row values
+// read from LDS into them), so no per-element row values stay in registers.
+// K' and V of the group are B operands read from LDS per chunk (fragment
+// order, linear reads) rather than held in registers; at D 128 the chunk
+// buffers are single (the next chunk is copied after every wave is done with
+// the current one) so that two workgroups fit a CU, each one's copies then
+// overlapping the other's products.
 // --------------------------------------------------------------------------
 template <int D, int TL>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 64 ? 2 : 1))) k_bwd_dkdv(BwdArgs a) {
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 64 ? 3 : 2))) k_bwd_dkdv(BwdArgs a) {
   using S = BShape<D>;
   constexpr int HALF = S::HALF, NKS = S::NKS, NDB = S::NDB;
   constexpr int QL = 2 * TL - 6, GPB = 1 << QL;   // chunks (64-row groups) per block
+  constexpr bool kSingle = D == 128;
   // Q, dO, lse2 and D buffers A and B (alternate chunks; query stream s of
-  // Q / dO at byte HALF s), separate variables as in k_bwd_dq.
+  // Q / dO at byte HALF s), separate variables as in k_bwd_dq; B unused
+  // (minimal) when single-buffered.
   __shared__ __attribute__((aligned(16))) char qA[2 * HALF];
-  __shared__ __attribute__((aligned(16))) char qB[2 * HALF];
+  __shared__ __attribute__((aligned(16))) char qB[kSingle ? 16 : 2 * HALF];
   __shared__ __attribute__((aligned(16))) char gA[2 * HALF];
-  __shared__ __attribute__((aligned(16))) char gB[2 * HALF];
+  __shared__ __attribute__((aligned(16))) char gB[kSingle ? 16 : 2 * HALF];
   __shared__ __attribute__((aligned(16))) float lA[64];   // lse2 of the chunk's rows
-  __shared__ __attribute__((aligned(16))) float lB[64];
+  __shared__ __attribute__((aligned(16))) float lB[kSingle ? 4 : 64];
   __shared__ __attribute__((aligned(16))) float dA[64];   // D of the chunk's rows
-  __shared__ __attribute__((aligned(16))) float dB[64];
+  __shared__ __attribute__((aligned(16))) float dB[kSingle ? 4 : 64];
+  // K' and V fragments: fragment ks of key half kh at 1024 (NKS kh + ks),
+  // lane l's 16 bytes at 16 l.
+  __shared__ __attribute__((aligned(16))) char kst[2 * NKS * 1024];
+  __shared__ __attribute__((aligned(16))) char vst[2 * NKS * 1024];
   int bh, r;
   group_of<QL>(a, bh, r);
   const int b = bh / a.heads, h = bh - b * a.heads;
@@ -475,10 +518,13 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int kh = w & 1, qs = w >> 1, hw = lane >> 5, l32 = lane & 31;
+  const int tb = a.n_tiles;
 
-  // This lane's key row.  An image group is chunk kq of key block kj.
   const bool text_group = r < a.n_text_groups;
   const int g = r - a.n_text_groups, kj = g >> QL, kq = g & (GPB - 1);
+  const uint64_t mask_i = lane < tb ? a.kmask[(int64_t)bh * tb + lane] : 0ull;   // query block i's kept set
+
+  // This lane's key row.  An image group is chunk kq of key block kj.
   int krow;
   if (text_group) {
     const int kk = 64 * r + 32 * kh + l32;
@@ -495,8 +541,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
   if (text_group) {
     n_img = a.n_tiles << QL;
   } else {
-    const uint64_t m = lane < a.n_tiles ? a.kmask[(int64_t)bh * a.n_tiles + lane] : 0ull;
-    members = __ballot(((m >> kj) & 1ull) != 0ull);
+    members = __ballot(((mask_i >> kj) & 1ull) != 0ull);
     n_img = __popcll(members) << QL;
   }
   const int n = n_img + n_txt;
@@ -518,13 +563,20 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
     return -1 - next_txt++;
   };
 
-  // K and V rows of the lane's key as B operands (lane = key column).
-  bf16x8 kf[NKS], vf[NKS];
+  // K' (scaled, rounded) and V rows of the lane's key into LDS (stream-0
+  // waves; read after the first barrier).
+  if (qs == 0) {
 #pragma unroll
-  for (int ks = 0; ks < NKS; ++ks) {
-    kf[ks] = *reinterpret_cast<const bf16x8*>(kbase + (int64_t)kr * st + 16 * ks + 8 * hw);
-    vf[ks] = *reinterpret_cast<const bf16x8*>(vbase + (int64_t)kr * st + 16 * ks + 8 * hw);
+    for (int ks = 0; ks < NKS; ++ks) {
+      const bf16x8 kraw = *reinterpret_cast<const bf16x8*>(kbase + (int64_t)kr * st + 16 * ks + 8 * hw);
+      const bf16x8 vraw = *reinterpret_cast<const bf16x8*>(vbase + (int64_t)kr * st + 16 * ks + 8 * hw);
+      *reinterpret_cast<bf16x8*>(kst + 1024 * (NKS * kh + ks) + 16 * lane) =
+          __builtin_convertvector(__builtin_convertvector(kraw, floatx8) * a.scale_log2, bf16x8);
+      *reinterpret_cast<bf16x8*>(vst + 1024 * (NKS * kh + ks) + 16 * lane) = vraw;
+    }
   }
+  const char* kfr = kst + 1024 * NKS * kh + 16 * lane;
+  const char* vfr = vst + 1024 * NKS * kh + 16 * lane;
 
   const unsigned slice_bytes = 2u * (unsigned)((a.seq - 1) * st + D);
   const __amdgpu_buffer_rsrc_t rq =
@@ -558,33 +610,30 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
   if (n > 0) issue(src, qA, gA, lA, dA);
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
   __syncthreads();
-  // Chunk c from the buffers (qc, gc, lc, dc) while chunk c + 1 is copied
-  // into the others.
-  auto body = [&](int c, const char* qc, const char* gc, const float* lc, const float* dc,
-                  char* qn, char* gn, float* ln, float* dn) {
-    const int nsrc = c + 1 < n ? pop_src() : 0;
-    if (c + 1 < n) issue(nsrc, qn, gn, ln, dn);
+  // The products of one chunk from the buffers (qc, gc, lc, dc).
+  auto compute = [&](const char* qc, const char* gc, const float* lc, const float* dc) {
     const char* qt = qc + HALF * qs;
     const char* gt = gc + HALF * qs;
     // Valid queries of this stream's half (text chunks end at n_text).
     int hi = 32;
     if (src < 0) hi = min(max(a.f.n_text - (64 * (-1 - src) + 32 * qs), 0), 32);
-    // Row values: element e of the lane's tile is query 8 (e / 4) + 4 hw + e % 4.
-    float nl[16], dl[16];
+    // Accumulators seeded with the row values: element e of the lane's tile
+    // is query 8 (e / 4) + 4 hw + e % 4.
+    floatx16 sc, dp;
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const float4 x = *reinterpret_cast<const float4*>(&lc[32 * qs + 8 * g + 4 * hw]);
-      const float4 y = *reinterpret_cast<const float4*>(&dc[32 * qs + 8 * g + 4 * hw]);
-      nl[4 * g] = -x.x; nl[4 * g + 1] = -x.y; nl[4 * g + 2] = -x.z; nl[4 * g + 3] = -x.w;
-      dl[4 * g] = y.x; dl[4 * g + 1] = y.y; dl[4 * g + 2] = y.z; dl[4 * g + 3] = y.w;
+    for (int gg = 0; gg < 4; ++gg) {
+      const float4 x = *reinterpret_cast<const float4*>(&lc[32 * qs + 8 * gg + 4 * hw]);
+      const float4 y = *reinterpret_cast<const float4*>(&dc[32 * qs + 8 * gg + 4 * hw]);
+      sc[4 * gg] = -x.x; sc[4 * gg + 1] = -x.y; sc[4 * gg + 2] = -x.z; sc[4 * gg + 3] = -x.w;
+      dp[4 * gg] = -y.x; dp[4 * gg + 1] = -y.y; dp[4 * gg + 2] = -y.z; dp[4 * gg + 3] = -y.w;
     }
-    floatx16 sc = floatx16{}, dp = floatx16{};
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
-      sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<D>(qt, lane, ks), kf[ks], sc, 0, 0, 0);
-      dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<D>(gt, lane, ks), vf[ks], dp, 0, 0, 0);
+      sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<D>(qt, lane, ks),
+                                                   *reinterpret_cast<const bf16x8*>(kfr + 1024 * ks), sc, 0, 0, 0);
+      dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<D>(gt, lane, ks),
+                                                   *reinterpret_cast<const bf16x8*>(vfr + 1024 * ks), dp, 0, 0, 0);
     }
-    // The chunk's rows carry Q itself: the product is scaled here.
     if (hi < 32) {   // rare: text tail
       int h4 = hi - 4 * hw;
       asm volatile("" : "+v"(h4));
@@ -595,13 +644,13 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
     uint32_t pp[8], pd[8];
 #pragma unroll
     for (int rr = 0; rr < 16; rr += 2) {
-      float p[2], ds[2];
+      float pr[2], ds[2];
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        p[u] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[rr + u], a.scale_log2, nl[rr + u]));
-        ds[u] = p[u] * (dp[rr + u] - dl[rr + u]);
+        pr[u] = __builtin_amdgcn_exp2f(sc[rr + u]);
+        ds[u] = pr[u] * dp[rr + u];
       }
-      pp[rr >> 1] = pack2(p[0], p[1]);
+      pp[rr >> 1] = pack2(pr[0], pr[1]);
       pd[rr >> 1] = pack2(ds[0], ds[1]);
     }
 #pragma unroll
@@ -615,21 +664,45 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
                                                         db8, dk[db], 0, 0, 0);
       }
     }
-    __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_waitcnt(kWaitVm0);
-    __syncthreads();
-    src = nsrc;
   };
-  for (int c = 0; c < n; c += 2) {
-    body(c, qA, gA, lA, dA, qB, gB, lB, dB);
-    if (c + 1 < n) body(c + 1, qB, gB, lB, dB, qA, gA, lA, dA);
+  if constexpr (kSingle) {
+    // Chunk c, then (every wave past it) the copy of chunk c + 1 into the
+    // same buffers.
+    for (int c = 0; c < n; ++c) {
+      compute(qA, gA, lA, dA);
+      __builtin_amdgcn_sched_barrier(0);
+      __syncthreads();
+      if (c + 1 < n) {
+        src = pop_src();
+        issue(src, qA, gA, lA, dA);
+      }
+      __builtin_amdgcn_s_waitcnt(kWaitVm0);
+      __syncthreads();
+    }
+  } else {
+    // Chunk c from one buffer set while chunk c + 1 is copied into the other.
+    auto body = [&](int c, const char* qc, const char* gc, const float* lc, const float* dc,
+                    char* qn, char* gn, float* ln, float* dn) {
+      const int nsrc = c + 1 < n ? pop_src() : 0;
+      if (c + 1 < n) issue(nsrc, qn, gn, ln, dn);
+      compute(qc, gc, lc, dc);
+      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_waitcnt(kWaitVm0);
+      __syncthreads();
+      src = nsrc;
+    };
+    for (int c = 0; c < n; c += 2) {
+      body(c, qA, gA, lA, dA, qB, gB, lB, dB);
+      if (c + 1 < n) body(c + 1, qB, gB, lB, dB, qA, gA, lA, dA);
+    }
   }
 
-  // Merge the two query streams through LDS (the Q / dO buffers are free):
-  // key half kh uses buffers A or B.
-  static_assert(16 * NDB * 64 * 4 <= 2 * HALF, "merge area fits one buffer");
-  float* xk = reinterpret_cast<float*>(kh ? qB : qA);
-  float* xv = reinterpret_cast<float*>(kh ? gB : gA);
+  // Merge the two query streams through LDS (every buffer is free now): key
+  // half 0 uses the Q and dO chunk buffers, key half 1 the K' and V ones.
+  static_assert(16 * NDB * 64 * 4 <= 2 * HALF && 16 * NDB * 64 * 4 <= 2 * NKS * 1024,
+                "merge area fits the buffers");
+  float* xk = reinterpret_cast<float*>(kh ? kst : qA);
+  float* xv = reinterpret_cast<float*>(kh ? vst : gA);
   if (qs == 1) {
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
