@@ -150,10 +150,12 @@ __shared__ int gate_list[64];
 // from the head's pooled key sums copied contiguously into the four buffers
 // (channel row c of T_b values in buffer c / (D/4)).  STRIDE = 64 gives every
 // read a constant offset; 0 reads with the runtime row length tb.  Lanes past
-// tb read a neighbouring row and are discarded by the caller.
+// tb read a neighbouring row and are discarded by the caller.  At D 64 the
+// pooled query sum of channel c is taken from lane c's `qreg` (the wave that
+// formed it) as a scalar operand, which leaves one LDS read per channel.
 template <int D, int STRIDE>
 __device__ __forceinline__ double affinity(const double* qsum, const char* b0, const char* b1,
-                                           const char* b2, const char* b3, int lane, int tb) {
+                                           const char* b2, const char* b3, int lane, int tb, double qreg) {
   constexpr int CPQ = D / 4;
   const int row = STRIDE ? STRIDE : tb;
   double s = 0.0;
@@ -162,7 +164,16 @@ __device__ __forceinline__ double affinity(const double* qsum, const char* b0, c
     const int qi = c / CPQ, cc = c % CPQ;
     const char* src = qi == 0 ? b0 : qi == 1 ? b1 : qi == 2 ? b2 : b3;
     const double kv = reinterpret_cast<const double*>(src)[cc * row + lane];
-    const double p = __dmul_rn(qsum[c], kv);
+    double qc;
+    if constexpr (D == 64) {
+      const uint64_t qbits = (uint64_t)__double_as_longlong(qreg);
+      const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)qbits, c);
+      const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(qbits >> 32), c);
+      qc = __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+    } else {
+      qc = qsum[c];
+    }
+    const double p = __dmul_rn(qc, kv);
     s = (c == 0) ? p : __dadd_rn(s, p);
   }
   return s;
@@ -232,8 +243,8 @@ __device__ __forceinline__ int gate_block(const AttnArgs& a, int bh, int i, int 
   // 3. affinity row and ranking (wave 0).
   if (w == 0) {
     const bool valid = lane < tb;
-    const double s = tb == 64 ? affinity<D, 64>(qsum, b0, b1, b2, b3, lane, tb)
-                              : affinity<D, 0>(qsum, b0, b1, b2, b3, lane, tb);
+    const double s = tb == 64 ? affinity<D, 64>(qsum, b0, b1, b2, b3, lane, tb, qacc)
+                              : affinity<D, 0>(qsum, b0, b1, b2, b3, lane, tb, qacc);
     const uint64_t key = valid ? rank_key(s) : 0;
     const bool kept = wave_topk(key, valid, a.keep, lane);
     const uint64_t km = __builtin_amdgcn_ballot_w64(kept);
