@@ -74,6 +74,15 @@ int main(void) {
     CHECK(ssba_forward_topk_ex(&d, fake, fake, fake, (int32_t*)fake, ib, fake, sb - 1, fake, NULL) ==
           SSBA_ERR_WORKSPACE);
     CHECK(ssba_forward_topk_ex(&d, NULL, fake, fake, (int32_t*)fake, ib, fake, sb, fake, NULL) == SSBA_ERR_ARG);
+    /* the fused call's two launches, one at a time */
+    CHECK(ssba_pool_keys_ex(&d, fake, fake, sb - 1, NULL) == SSBA_ERR_WORKSPACE);
+    CHECK(ssba_pool_keys_ex(&d, NULL, fake, sb, NULL) == SSBA_ERR_ARG);
+    CHECK(ssba_forward_gated_ex(&d, fake, fake, fake, (int32_t*)fake, ib - 1, fake, sb, fake, NULL) ==
+          SSBA_ERR_WORKSPACE);
+    CHECK(ssba_forward_gated_ex(&d, fake, fake, NULL, (int32_t*)fake, ib, fake, sb, fake, NULL) == SSBA_ERR_ARG);
+    d.tile = 16;
+    CHECK(ssba_pool_keys_ex(&d, fake, fake, (size_t)1 << 30, NULL) == SSBA_ERR_UNSUPPORTED);
+    d.tile = 8;
   }
   CHECK(ssba_forward_kernel(&d, 7) == NULL);
 

@@ -128,6 +128,19 @@ int main() {
     CHECK(std::strcmp(stub_calls()[0].what, "pool_keys") == 0);
     CHECK(stub_calls()[1].scratch == static_cast<char*>(scr) + (size_t)8 * 16 * 64 * 64);
 
+    // the same two launches one at a time
+    stub_calls().clear();
+    CHECK(ssba_pool_keys_ex(&d, b.k.data(), scr, sb - 1, nullptr) == SSBA_ERR_WORKSPACE);
+    CHECK(ssba_forward_gated_ex(&d, b.q.data(), b.k.data(), b.v.data(), idx, ib - 1, scr, sb, b.o.data(),
+                                nullptr) == SSBA_ERR_WORKSPACE);
+    CHECK(stub_calls().empty());
+    CHECK(ssba_pool_keys_ex(&d, b.k.data(), scr, sb, nullptr) == SSBA_OK);
+    CHECK(ssba_forward_gated_ex(&d, b.q.data(), b.k.data(), b.v.data(), idx, ib, scr, sb, b.o.data(), nullptr) ==
+          SSBA_OK);
+    CHECK(stub_calls().size() == 2 && std::strcmp(stub_calls()[0].what, "pool_keys") == 0);
+    CHECK(stub_calls()[1].gated == 1 && stub_calls()[1].index == idx &&
+          stub_calls()[1].scratch == static_cast<char*>(scr) + (size_t)8 * 16 * 64 * 64);
+
     // misaligned and missing pointers
     CHECK(ssba_forward_ex(&d, static_cast<char*>(static_cast<void*>(b.q.data())) + 2, b.k.data(), b.v.data(), idx,
                           ib, b.o.data(), nullptr) == SSBA_ERR_ARG);
