@@ -200,7 +200,10 @@ template <int D, int NKS>
 __device__ __forceinline__ int gate_block(const AttnArgs& a, int bh, int i, int w, int lane, const bf16x8 (&qf)[NKS],
                                           char* b0, char* b1, char* b2, char* b3) {
   __shared__ double qsum[D];
-  __shared__ __attribute__((aligned(16))) char qstage[32 * 2 * D];   // 32 query rows
+  // 32 query rows, each padded by 16 bytes so that the 16-byte writes of
+  // consecutive rows start on different banks.
+  constexpr int QROW = 2 * D + 16;
+  __shared__ __attribute__((aligned(16))) char qstage[32 * QROW];
   const int tb = a.n_tiles;
   const int quarter_bytes = 2 * D * tb;   // D * tb * 8 / 4
   // 1. pooled key sums of this (batch, head): wave w copies quarter w.
@@ -225,14 +228,14 @@ __device__ __forceinline__ int gate_block(const AttnArgs& a, int bh, int i, int 
       const int row = lane & 31, hw = lane >> 5;
 #pragma unroll
       for (int ks = 0; ks < NKS; ++ks)
-        *reinterpret_cast<bf16x8*>(qstage + row * 2 * D + 32 * ks + 16 * hw) = qf[ks];
+        *reinterpret_cast<bf16x8*>(qstage + row * QROW + 32 * ks + 16 * hw) = qf[ks];
     }
     __syncthreads();
     if (tid < D) {
       float xs[32];
 #pragma unroll
       for (int r = 0; r < 32; ++r)
-        xs[r] = __uint_as_float((uint32_t)*reinterpret_cast<const uint16_t*>(qstage + r * 2 * D + 2 * tid) << 16);
+        xs[r] = __uint_as_float((uint32_t)*reinterpret_cast<const uint16_t*>(qstage + r * QROW + 2 * tid) << 16);
 #pragma unroll
       for (int r = 0; r < 32; ++r) qacc = (half == 0 && r == 0) ? (double)xs[r] : __dadd_rn(qacc, (double)xs[r]);
     }
