@@ -398,10 +398,12 @@ def measured_mfma_tflops(blocks: int = 1024, iters: int = 2000, reps: int = 3) -
     return blocks * 4 * iters * 8 * 32768 / (best * 1e-3) / 1e12
 
 
-def measure_layers(w, steps: int, warmup: int) -> dict:
+def measure_layers(w, steps: int, warmup: int, settle_ms: float = 0.0) -> dict:
     """A 24-layer stack through ssba_forward_layers: the synthetic per-layer
     keep schedule, the offset alternating by layer parity, every layer with
-    its own seeded Q, K, V (so the stack's 768 MB do not fit the MALL)."""
+    its own seeded Q, K, V (so the stack's 768 MB do not fit the MALL).  The
+    stack and the same layers as separate calls are timed in alternation,
+    REPEATS rounds, median of each, after the clock-settle phase."""
     import torch
     from paper_2605_15684_amd import ssba
     from paper_2605_15684_amd.inputs import LAYER_KEEP_SCHEDULE_24, LAYER_SKIP_24, make_qkv
@@ -426,7 +428,8 @@ def measure_layers(w, steps: int, warmup: int) -> dict:
         return e0.elapsed_time(e1) / n
 
     index, scratch = ssba.forward_layers(layers, desc)
-    ms_stack = span(lambda: ssba.forward_layers(layers, desc, index, scratch), steps)
+    stack = lambda: ssba.forward_layers(layers, desc, index, scratch)
+    settle_calls = settle_clock(stack, settle_ms) if settle_ms > 0 else 0
 
     # The same layers as 24 separate fused calls from Python.
     per = []
@@ -439,7 +442,12 @@ def measure_layers(w, steps: int, warmup: int) -> dict:
     def separate():
         for L, dl, il, sl in per:
             ssba.forward_topk(L["q"], L["k"], L["v"], dl, il, sl, L["out"])
-    ms_separate = span(separate, steps)
+    rounds = {"stack": [], "separate": []}
+    for _ in range(REPEATS):
+        rounds["stack"].append(span(stack, steps))
+        rounds["separate"].append(span(separate, steps))
+    ms_stack = statistics.median(rounds["stack"])
+    ms_separate = statistics.median(rounds["separate"])
 
     # Depth-pruned stack: the skip mask of the bench (6 of 24 layers skipped).
     pruned = [dict(L, skip=sk) for L, sk in zip(layers, LAYER_SKIP_24)]
@@ -467,6 +475,7 @@ def measure_layers(w, steps: int, warmup: int) -> dict:
         "steps": steps, "warmup": warmup, "ms_per_step": round(ms_stack, 5), "higher_is_better": True,
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"{w.name} x 24 layers: {describe(w)} (keep per layer {list(keeps)})"},
+        "clock_settle_ms": settle_ms, "clock_settle_calls": settle_calls,
         "ms_per_layer": round(ms_stack / len(keeps), 5),
         "ms_separate_fused_calls": round(ms_separate, 5),
         "ms_pruned_stack": round(ms_pruned, 5), "pruned_layers_skipped": int(sum(LAYER_SKIP_24)),
@@ -676,7 +685,8 @@ def main():
         print(json.dumps(measure_backward(w, args.steps, args.warmup)), flush=True)
         return
     if args.layers:
-        print(json.dumps(measure_layers(w, max(5, args.steps // 10), max(2, args.warmup // 10))), flush=True)
+        print(json.dumps(measure_layers(w, max(5, args.steps // 10), max(2, args.warmup // 10),
+                                        settle_ms=args.settle_ms)), flush=True)
         return
     r, m = measure(w, args.steps, args.warmup, max(20, args.steps // 4), settle_ms=args.settle_ms)
     f = flops(w)
