@@ -90,11 +90,11 @@ MEASURED_TRAFFIC = {
     ("k_haar_dwt<unsigned short, 3>", "haar512"): {"sha": "02be9c317bd1aa8b", "fetch_kib": 131115.0,
                                                   "write_kib": 344064.0, "fetch_factor": 1.9998,
                                                   "write_factor": 1.0},
-    ("k_attn_mfma<64, 3, false, true>", "grid64"): {"sha": "d4b42431e57f849e", "fetch_kib": 12665.5,
-                                                    "write_kib": 8456.0, "fetch_factor": 1.99983,
+    ("k_attn_mfma<64, 3, false, true>", "grid64"): {"sha": "aace8cb566779fe3", "fetch_kib": 12666.0,
+                                                    "write_kib": 8456.0, "fetch_factor": 1.99985,
                                                     "write_factor": 1.0},
-    ("k_attn_mfma<64, 3, false, false>", "grid64"): {"sha": "d4b42431e57f849e", "fetch_kib": 12551.0,
-                                                     "write_kib": 8192.0, "fetch_factor": 1.99983,
+    ("k_attn_mfma<64, 3, false, false>", "grid64"): {"sha": "aace8cb566779fe3", "fetch_kib": 12553.1,
+                                                     "write_kib": 8192.0, "fetch_factor": 1.99985,
                                                      "write_factor": 1.0},
 }
 
