@@ -151,7 +151,7 @@ __device__ __forceinline__ void swizzle_offsets(int sub, int lane, unsigned (&zo
 // column depends on the lane.
 template <int D, int TL>
 __device__ __forceinline__ void copy_offsets(const Frame& f, int src, int hf, int sub, unsigned st2,
-                                             const unsigned (&zoff)[BShape<D>::NIW], int lane,
+                                             const unsigned (&zoff)[BShape<D>::NIW],
                                              unsigned (&off)[BShape<D>::NIW]) {
   using S = BShape<D>;
   constexpr int TILE = 1 << TL, QL = 2 * TL - 6;
@@ -161,7 +161,6 @@ __device__ __forceinline__ void copy_offsets(const Frame& f, int src, int hf, in
   int ln = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
   asm volatile("" : "+v"(ln));
   const int kin = ln / S::CPR;
-  (void)lane;
   if (src >= 0) {
     const int blk = src >> QL, quarter = src & ((1 << QL) - 1);
     const int ty = blk / f.nx, tx = blk - ty * f.nx;
@@ -361,7 +360,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
   auto issue = [&](int c, char* kd, char* vd) {
     const int src = src_of(c);
     unsigned offs[S::NIW];
-    copy_offsets<D, TL>(a.f, src == -1000000 ? 0 : src, sk, qh, 2u * (unsigned)st, zoff, lane, offs);
+    copy_offsets<D, TL>(a.f, src == -1000000 ? 0 : src, sk, qh, 2u * (unsigned)st, zoff, offs);
     copy_half<D>(rk, offs, qh, kd + HALF * sk);
     copy_half<D>(rv, offs, qh, vd + HALF * sk);
   };
@@ -592,7 +591,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
   swizzle_offsets<D>(kh, lane, zoff);
   auto issue = [&](int src, char* qd, char* gd, float* ld, float* dd) {
     unsigned offs[S::NIW];
-    copy_offsets<D, TL>(a.f, src, qs, kh, 2u * (unsigned)st, zoff, lane, offs);
+    copy_offsets<D, TL>(a.f, src, qs, kh, 2u * (unsigned)st, zoff, offs);
     copy_half<D>(rq, offs, kh, qd + HALF * qs);
     copy_half<D>(rg, offs, kh, gd + HALF * qs);
     if (w == 0) copy_rowvals<QL>(rl, a.f, src, ld, lane);
