@@ -513,6 +513,47 @@ ssba_status ssba_forward_layers_ex(const ssba_desc* d, const ssba_layer* layers,
   const size_t scr_stride = layer_scratch_stride(&base, s);
   if (index_bytes / idx_bytes < (size_t)n_layers || scratch_bytes / scr_stride < (size_t)n_layers)
     return SSBA_ERR_WORKSPACE;
+  if (d->gate == SSBA_GATE_TOPK && gated_supported(&base, s)) {
+    // The fused form with its pooling pre-pass batched: one launch pools the
+    // keys of up to kPoolLayersMax layers into their scratch slices, then
+    // each layer's gated attention launch reads its slice.  Same kernels and
+    // arithmetic as one ssba_forward_topk call per layer, so the same bits.
+    ssba_desc odd = base;
+    odd.shift_y = -d->shift_y;
+    odd.shift_x = -d->shift_x;
+    Shape so;
+    st = check_desc(&odd, &so);
+    if (st != SSBA_OK) return st;
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    for (int l0 = 0; l0 < n_layers;) {
+      ssba::PoolLayers p;
+      std::memset(&p, 0, sizeof(p));
+      p.a = index_args(&base, s, nullptr, nullptr, nullptr, scratch);
+      p.f[0] = s.f;
+      p.f[1] = so.f;
+      int np = 0, l1 = l0;
+      for (; l1 < n_layers && np < ssba::kPoolLayersMax; ++l1) {
+        if (layers[l1].skip) continue;
+        p.k[np] = layers[l1].k;
+        p.kb[np] = index_args(&base, s, nullptr, nullptr, nullptr,
+                              static_cast<char*>(scratch) + (size_t)l1 * scr_stride).kb;
+        p.parity[np] = l1 & 1;
+        ++np;
+      }
+      if (np > 0 && ssba::launch_pool_keys_layers(p, np, hs) != hipSuccess) return SSBA_ERR_HIP;
+      for (int l = l0; l < l1; ++l) {
+        const ssba_layer& L = layers[l];
+        if (L.skip) continue;
+        ssba_desc dl = (l & 1) ? odd : base;
+        dl.keep = L.keep;
+        st = ssba_forward_gated_ex(&dl, L.q, L.k, L.v, index + (size_t)l * idx_elems, idx_bytes,
+                                   static_cast<char*>(scratch) + (size_t)l * scr_stride, scr_stride, L.o, stream);
+        if (st != SSBA_OK) return st;
+      }
+      l0 = l1;
+    }
+    return SSBA_OK;
+  }
   int cached[2] = {-1, -1};   // static gates: the layer whose index serves each parity
   for (int l = 0; l < n_layers; ++l) {
     const ssba_layer& L = layers[l];

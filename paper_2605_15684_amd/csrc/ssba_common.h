@@ -134,11 +134,26 @@ struct BwdArgs {
   float scale, scale_log2;
 };
 
+// The pooled-key pre-pass of up to kPoolLayersMax layers in one launch (the
+// layer driver): layer y pools K at k[y] into kb[y] in the frame
+// f[parity[y]] (the shift alternates sign between layers); every other
+// field is a's.
+constexpr int kPoolLayersMax = 32;
+struct PoolLayers {
+  IndexArgs a;
+  Frame f[2];
+  const void* k[kPoolLayersMax];
+  double* kb[kPoolLayersMax];
+  int parity[kPoolLayersMax];
+};
+
 // Launchers (each returns hipGetLastError() of its launch).
 hipError_t launch_pool(const IndexArgs& a, int dtype, hipStream_t s);
 // Pooled key sums only (bf16, 8x8 blocks): the pre-pass of the gated attention
 // kernel, which forms the pooled query sums itself.
 hipError_t launch_pool_keys(const IndexArgs& a, hipStream_t s);
+// The same for n_layers <= kPoolLayersMax layers of one shape.
+hipError_t launch_pool_keys_layers(const PoolLayers& p, int n_layers, hipStream_t s);
 hipError_t launch_gate_topk(const IndexArgs& a, hipStream_t s);
 // Head-shared top-k gate: per-head affinity rows, then their sum over heads.
 hipError_t launch_gate_topk_shared(const IndexArgs& a, hipStream_t s);

@@ -46,7 +46,7 @@ __device__ __forceinline__ void unit_of(const IndexArgs& a, int& t, int& h, int&
 // [B][H][T_b][D]; pooled k channel-major [B][H][D][T_b], so that the gate
 // reads one channel of all key blocks with one coalesced load.
 template <int DTYPE, int TILE_LOG2, int D, int NT>
-__global__ void __launch_bounds__(256) k_pool(IndexArgs a) {
+__device__ __forceinline__ void pool_block(const IndexArgs& a) {
   constexpr int SLOTS = 1 << (2 * TILE_LOG2);
   constexpr int SB = SLOTS < 64 ? SLOTS : 64;          // slots per stage
   constexpr bool BF16 = DTYPE == SSBA_DT_BF16;
@@ -105,6 +105,22 @@ __global__ void __launch_bounds__(256) k_pool(IndexArgs a) {
     else
       a.kb[(bh * D + c) * a.n_tiles + t] = sum;
   }
+}
+
+template <int DTYPE, int TILE_LOG2, int D, int NT>
+__global__ void __launch_bounds__(256) k_pool(IndexArgs a) {
+  pool_block<DTYPE, TILE_LOG2, D, NT>(a);
+}
+
+// Pooled key sums of several layers (grid y = layer), bf16, 8x8 blocks.
+template <int D>
+__global__ void __launch_bounds__(256) k_pool_keys_layers(PoolLayers p) {
+  const int l = blockIdx.y;
+  IndexArgs a = p.a;
+  a.k = p.k[l];
+  a.kb = p.kb[l];
+  a.f = p.f[p.parity[l] & 1];
+  pool_block<SSBA_DT_BF16, 3, D, 1>(a);
 }
 
 // S[i][j] of one (batch, head): the channel-ordered sum of the rounded
@@ -312,6 +328,16 @@ hipError_t launch_pool_keys(const IndexArgs& a, hipStream_t s) {
   dim3 grid(a.n_tiles * a.heads * a.batch), block(256);
   if (a.head_dim == 64) hipLaunchKernelGGL((k_pool<SSBA_DT_BF16, 3, 64, 1>), grid, block, 0, s, a);
   else hipLaunchKernelGGL((k_pool<SSBA_DT_BF16, 3, 128, 1>), grid, block, 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_pool_keys_layers(const PoolLayers& p, int n_layers, hipStream_t s) {
+  if (p.a.f.tile_log2 != 3 || p.f[0].tile_log2 != 3 || p.f[1].tile_log2 != 3 || n_layers < 1 ||
+      n_layers > kPoolLayersMax)
+    return hipErrorInvalidValue;
+  dim3 grid(p.a.n_tiles * p.a.heads * p.a.batch, n_layers), block(256);
+  if (p.a.head_dim == 64) hipLaunchKernelGGL((k_pool_keys_layers<64>), grid, block, 0, s, p);
+  else hipLaunchKernelGGL((k_pool_keys_layers<128>), grid, block, 0, s, p);
   return hipGetLastError();
 }
 

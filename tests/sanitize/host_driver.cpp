@@ -197,17 +197,51 @@ int main() {
     CHECK(ssba_forward_layers_ex(&d, layers, L, idx, lib, scr, lsb - 1, nullptr) == SSBA_ERR_WORKSPACE);
     CHECK(stub_calls().empty());
     CHECK(ssba_forward_layers_ex(&d, layers, L, idx, lib, scr, lsb, nullptr) == SSBA_OK);
-    // four layers ran, each as pool + gated attention
+    // four layers ran: one pooling pre-pass over their keys, then each
+    // layer's gated attention
     CHECK(stub_calls().size() == 8);
     const int ran[] = {0, 1, 3, 4};
+    const size_t pooled = (size_t)8 * 16 * 64 * 64;   // the pooled key sums follow 8 B H T_b D bytes of q sums
     for (int i = 0; i < 4; ++i) {
       const int l = ran[i];
-      const StubCall& att = stub_calls()[2 * i + 1];
+      const StubCall& pre = stub_calls()[i];
+      CHECK(std::strcmp(pre.what, "pool_keys_layers") == 0 && pre.index == layers[l].k);
+      CHECK(pre.scratch == scr + (size_t)l * stride + pooled && pre.keep == (l & 1));
+      const StubCall& att = stub_calls()[4 + i];
       CHECK(att.gated == 1 && att.keep == 3 + l);
       CHECK(att.index == idx + (size_t)l * (ib / 4));
-      CHECK(stub_calls()[2 * i].scratch == scr + (size_t)l * stride);
+      CHECK(att.scratch == pre.scratch);
       // offsets alternate sign: +4 on even layers, -4 (reduced: 60) on odd ones
       CHECK(att.sy == ((l & 1) ? 60 : 4) && att.sx == att.sy);
+      CHECK(pre.sy == att.sy && pre.sx == att.sx);
+    }
+    // more layers than one pre-pass launch takes: launches of at most 32
+    {
+      const int LL = 70;
+      size_t lib2 = 0, lsb2 = 0;
+      CHECK(ssba_layers_workspace_size(&d, LL, &lib2, &lsb2) == SSBA_OK);
+      Buffers b2(tensor, lib2, lsb2);
+      std::vector<ssba_layer> many(LL);
+      for (int l = 0; l < LL; ++l) {
+        many[l] = layers[0];
+        many[l].keep = 1 + l % 64;
+        many[l].skip = (l % 5 == 4) ? 1 : 0;
+      }
+      stub_calls().clear();
+      CHECK(ssba_forward_layers_ex(&d, many.data(), LL, reinterpret_cast<int32_t*>(b2.index.data()), lib2,
+                                   b2.scratch.data(), lsb2, nullptr) == SSBA_OK);
+      int pre = 0, att = 0, run = 0, longest = 0;
+      for (const StubCall& c : stub_calls()) {
+        if (std::strcmp(c.what, "pool_keys_layers") == 0) {
+          ++pre;
+          ++run;
+          longest = run > longest ? run : longest;
+        } else {
+          ++att;
+          run = 0;
+        }
+      }
+      CHECK(pre == 56 && att == 56 && longest == 32);
     }
     // static gate: the index is built once per offset parity
     ssba_desc w = d;

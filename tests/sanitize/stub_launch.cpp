@@ -27,6 +27,15 @@ hipError_t rec_attn(const char* what, const AttnArgs& a) {
 
 hipError_t launch_pool(const IndexArgs& a, int, hipStream_t) { return rec_index("pool", a); }
 hipError_t launch_pool_keys(const IndexArgs& a, hipStream_t) { return rec_index("pool_keys", a); }
+// One record per layer: its pooled-key slice, parity (in keep) and frame offsets.
+hipError_t launch_pool_keys_layers(const PoolLayers& p, int n_layers, hipStream_t) {
+  if (n_layers < 1 || n_layers > kPoolLayersMax) return hipErrorInvalidValue;
+  for (int i = 0; i < n_layers; ++i) {
+    const Frame& f = p.f[p.parity[i] & 1];
+    stub_calls().push_back({"pool_keys_layers", p.k[i], p.kb[i], nullptr, nullptr, p.parity[i], f.sy, f.sx, 0});
+  }
+  return hipSuccess;
+}
 hipError_t launch_gate_topk(const IndexArgs& a, hipStream_t) { return rec_index("gate_topk", a); }
 hipError_t launch_gate_topk_shared(const IndexArgs& a, hipStream_t) { return rec_index("gate_shared", a); }
 hipError_t launch_gate_static(const IndexArgs& a, int, hipStream_t) { return rec_index("gate_static", a); }

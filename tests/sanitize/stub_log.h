@@ -5,8 +5,8 @@
 
 struct StubCall {
   const char* what;       // launcher name
-  const void* index;      // index read or written
-  const void* scratch;    // pooled sums (q for the gates, k for the attention), backward lse2
+  const void* index;      // index read or written (the layer pre-pass: the keys pooled)
+  const void* scratch;    // pooled sums (q for the gates, k for the attention and the layer pre-pass), backward lse2
   const void* flags;      // status flags (gates) / kept-block masks (backward)
   const void* out;        // attention output
   int keep, sy, sx, gated;

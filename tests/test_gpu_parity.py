@@ -433,6 +433,32 @@ def test_layer_stack_equals_per_layer_calls(gate, window):
             assert ssba.read_status(dl_status, scratch[l]) == 0
 
 
+def test_layer_stack_beyond_one_prepass_launch():
+    """A stack longer than one batched pooling launch takes (32 layers), with
+    skipped layers and text tokens: every layer's index, status and output
+    equal one fused call per layer."""
+    from paper_2605_15684_amd import ssba
+    w = preset("grid64", heads=1, grid_h=32, grid_w=32, n_text=13, shift=(4, 4))
+    n = 37
+    keeps = [1 + (5 * l) % 16 for l in range(n)]
+    skips = [l % 6 == 5 for l in range(n)]
+    layers = _layer_stack(w, keeps, skips, seed0=100)
+    desc = gpu_desc(w, layers[0]["q"])
+    index, scratch = ssba.forward_layers(layers, desc)
+    torch.cuda.synchronize()
+    for l, L in enumerate(layers):
+        if L["skip"]:
+            assert bool((L["out"] == 7.0).all())
+            continue
+        wl = w.with_(shift=(4, 4) if l % 2 == 0 else (-4, -4), keep=keeps[l])
+        dl = gpu_desc(wl, L["q"])
+        idx1, _, out1 = ssba.forward_topk(L["q"], L["k"], L["v"], dl)
+        torch.cuda.synchronize()
+        assert torch.equal(index[l], idx1), f"layer {l}"
+        assert torch.equal(L["out"], out1), f"layer {l}"
+        assert ssba.read_status(dl, scratch[l]) == 0
+
+
 def test_layer_stack_against_oracle_and_status():
     """Three layers at the 64x64 size against the oracle's layer stack
     (sampled rows), with a NaN in layer 1 reported by that layer's scratch
