@@ -514,10 +514,12 @@ ssba_status ssba_forward_layers_ex(const ssba_desc* d, const ssba_layer* layers,
   if (index_bytes / idx_bytes < (size_t)n_layers || scratch_bytes / scr_stride < (size_t)n_layers)
     return SSBA_ERR_WORKSPACE;
   if (d->gate == SSBA_GATE_TOPK && gated_supported(&base, s)) {
-    // The fused form with its pooling pre-pass batched: one launch pools the
-    // keys of up to kPoolLayersMax layers into their scratch slices, then
-    // each layer's gated attention launch reads its slice.  Same kernels and
-    // arithmetic as one ssba_forward_topk call per layer, so the same bits.
+    // The fused form, batched over layers: one launch pools the keys of up
+    // to 32 layers into their scratch slices, then one launch runs those
+    // layers' gated attention (grid y = layer), each reading its slice.
+    // Every workgroup does what it does in one ssba_forward_topk call per
+    // layer, so the indices, flags and outputs are the same bits.
+    static_assert(ssba::kPoolLayersMax == ssba::kAttnLayersMax, "one chunk of layers per launch pair");
     ssba_desc odd = base;
     odd.shift_y = -d->shift_y;
     odd.shift_x = -d->shift_x;
@@ -525,31 +527,38 @@ ssba_status ssba_forward_layers_ex(const ssba_desc* d, const ssba_layer* layers,
     st = check_desc(&odd, &so);
     if (st != SSBA_OK) return st;
     hipStream_t hs = static_cast<hipStream_t>(stream);
+    ssba::PoolLayers p;
+    ssba::AttnLayers at;
     for (int l0 = 0; l0 < n_layers;) {
-      ssba::PoolLayers p;
       std::memset(&p, 0, sizeof(p));
+      std::memset(&at, 0, sizeof(at));
       p.a = index_args(&base, s, nullptr, nullptr, nullptr, scratch);
-      p.f[0] = s.f;
-      p.f[1] = so.f;
+      p.f[0] = at.f[0] = s.f;
+      p.f[1] = at.f[1] = so.f;
+      at.a = attn_args(&base, s, nullptr, nullptr, nullptr, nullptr, nullptr, false);
+      at.a.gated = 1;
       int np = 0, l1 = l0;
       for (; l1 < n_layers && np < ssba::kPoolLayersMax; ++l1) {
-        if (layers[l1].skip) continue;
-        p.k[np] = layers[l1].k;
-        p.kb[np] = index_args(&base, s, nullptr, nullptr, nullptr,
-                              static_cast<char*>(scratch) + (size_t)l1 * scr_stride).kb;
-        p.parity[np] = l1 & 1;
+        const ssba_layer& L = layers[l1];
+        if (L.skip) continue;
+        const IndexArgs ia = index_args(&base, s, nullptr, nullptr, nullptr,
+                                        static_cast<char*>(scratch) + (size_t)l1 * scr_stride);
+        p.k[np] = L.k;
+        p.kb[np] = ia.kb;
+        p.parity[np] = at.parity[np] = l1 & 1;
+        at.q[np] = L.q;
+        at.k[np] = L.k;
+        at.v[np] = L.v;
+        at.o[np] = L.o;
+        at.kb[np] = ia.kb;
+        at.index_out[np] = index + (size_t)l1 * idx_elems;
+        at.flags[np] = ia.flags;
+        at.keep[np] = L.keep;
         ++np;
       }
-      if (np > 0 && ssba::launch_pool_keys_layers(p, np, hs) != hipSuccess) return SSBA_ERR_HIP;
-      for (int l = l0; l < l1; ++l) {
-        const ssba_layer& L = layers[l];
-        if (L.skip) continue;
-        ssba_desc dl = (l & 1) ? odd : base;
-        dl.keep = L.keep;
-        st = ssba_forward_gated_ex(&dl, L.q, L.k, L.v, index + (size_t)l * idx_elems, idx_bytes,
-                                   static_cast<char*>(scratch) + (size_t)l * scr_stride, scr_stride, L.o, stream);
-        if (st != SSBA_OK) return st;
-      }
+      if (np > 0 && (ssba::launch_pool_keys_layers(p, np, hs) != hipSuccess ||
+                     ssba::launch_attn_mfma_layers(at, np, d->head_dim, hs) != hipSuccess))
+        return SSBA_ERR_HIP;
       l0 = l1;
     }
     return SSBA_OK;

@@ -276,8 +276,7 @@ __device__ __forceinline__ int gate_block(const AttnArgs& a, int bh, int i, int 
 // GATED: each image group computes its block's top-k gate first (from the
 // pooled key sums) and writes the block's index row and status flag.
 template <int D, int TILE_LOG2, bool DENSE, bool GATED>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 64 ? 4 : GATED ? 2 : 3)))
-k_attn_mfma(AttnArgs a) {
+__device__ __forceinline__ void attn_mfma_body(const AttnArgs& a) {
   using S = Shape<D, TILE_LOG2>;
   constexpr int BT = S::BT, CPR = S::CPR, KPI = S::KPI, NIW = S::NIW, HALF = S::HALF;
   constexpr int CPB = S::CPB, GPB = S::GPB, NKS = S::NKS, NDB = S::NDB;
@@ -723,10 +722,35 @@ k_attn_mfma(AttnArgs a) {
   }
 }
 
-}  // namespace
+template <int D, int TILE_LOG2, bool DENSE, bool GATED>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 64 ? 4 : GATED ? 2 : 3)))
+k_attn_mfma(AttnArgs a) {
+  attn_mfma_body<D, TILE_LOG2, DENSE, GATED>(a);
+}
 
-hipError_t launch_attn_mfma(const AttnArgs& a0, int head_dim, int tile, hipStream_t s) {
-  AttnArgs a = a0;
+// Gated attention of several layers in one launch (grid y = layer): the
+// workgroups of layer l + 1 start as those of layer l finish, so one layer's
+// tail and the next one's start overlap.  Each workgroup runs exactly what
+// it runs in a one-layer launch.
+template <int D>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 64 ? 4 : 2)))
+k_attn_mfma_layers(AttnLayers p) {
+  const int l = blockIdx.y;
+  AttnArgs a = p.a;
+  a.q = p.q[l];
+  a.k = p.k[l];
+  a.v = p.v[l];
+  a.o = p.o[l];
+  a.kb = p.kb[l];
+  a.index_out = p.index_out[l];
+  a.flags = p.flags[l];
+  a.keep = p.keep[l];
+  a.f = p.f[p.parity[l] & 1];
+  attn_mfma_body<D, 3, false, true>(a);
+}
+
+// Image and text workgroup counts of a launch.
+void set_groups(AttnArgs& a, int tile) {
   const int gpb = (tile == 16) ? 4 : 1;   // 64-query groups per image block
   if (a.dense) {
     a.n_text_groups = (a.seq + 63) / 64;    // every group runs natural-order rows
@@ -737,6 +761,30 @@ hipError_t launch_attn_mfma(const AttnArgs& a0, int head_dim, int tile, hipStrea
     a.groups_per_tile = gpb;
     a.groups_per_bh = a.n_text_groups + a.n_tiles * gpb;
   }
+}
+
+}  // namespace
+
+hipError_t launch_attn_mfma_layers(const AttnLayers& p0, int n_layers, int head_dim, hipStream_t s) {
+  if (n_layers < 1 || n_layers > kAttnLayersMax || !p0.a.gated || p0.a.dense || p0.a.f.tile_log2 != 3 ||
+      (head_dim != 64 && head_dim != 128))
+    return hipErrorInvalidValue;
+  AttnLayers p = p0;
+  set_groups(p.a, 8);
+  // Several layers never fit the CUs at once: the chunk-count priorities
+  // stay off (they only pay when the whole grid is resident).
+  p.a.equalize = 0;
+  const int64_t per_layer = (int64_t)p.a.batch * p.a.heads * p.a.groups_per_bh;
+  if (per_layer <= 0) return hipSuccess;
+  const dim3 grid((unsigned)per_layer, (unsigned)n_layers), block(256);
+  if (head_dim == 64) hipLaunchKernelGGL((k_attn_mfma_layers<64>), grid, block, 0, s, p);
+  else hipLaunchKernelGGL((k_attn_mfma_layers<128>), grid, block, 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_mfma(const AttnArgs& a0, int head_dim, int tile, hipStream_t s) {
+  AttnArgs a = a0;
+  set_groups(a, tile);
   const int64_t total = (int64_t)a.batch * a.heads * a.groups_per_bh;
   if (total <= 0) return hipSuccess;
   // Resident workgroups per CU: four waves each, four (D 64), three (D 128

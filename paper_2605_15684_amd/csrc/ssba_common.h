@@ -100,6 +100,25 @@ struct AttnArgs {
   int equalize;
 };
 
+// Gated attention of up to kAttnLayersMax layers of one shape in one launch
+// (the layer driver): layer y reads q/k/v[y] and kb[y], writes o[y],
+// index_out[y] and flags[y], keeps keep[y] blocks, in frame f[parity[y]];
+// every other field is a's.
+constexpr int kAttnLayersMax = 32;
+struct AttnLayers {
+  AttnArgs a;
+  Frame f[2];
+  const void* q[kAttnLayersMax];
+  const void* k[kAttnLayersMax];
+  const void* v[kAttnLayersMax];
+  void* o[kAttnLayersMax];
+  const double* kb[kAttnLayersMax];
+  int32_t* index_out[kAttnLayersMax];
+  int32_t* flags[kAttnLayersMax];
+  int keep[kAttnLayersMax];
+  int parity[kAttnLayersMax];
+};
+
 struct IndexArgs {
   const void* q;
   const void* k;
@@ -164,6 +183,8 @@ hipError_t launch_attn_f32(const AttnArgs& a, int head_dim, int tile, hipStream_
 // gated launches (a.gated) need 8x8 blocks.
 bool mfma_supported(int head_dim, int tile, bool dense, int n_tiles, int seq, int64_t span);
 hipError_t launch_attn_mfma(const AttnArgs& a, int head_dim, int tile, hipStream_t s);
+// Gated attention (bf16, 8x8 blocks, D 64 or 128) of n_layers <= kAttnLayersMax layers.
+hipError_t launch_attn_mfma_layers(const AttnLayers& p, int n_layers, int head_dim, hipStream_t s);
 const char* mfma_kernel_name(int head_dim, int tile, bool dense, bool gated);
 // Backward: bf16, 8x8 or 16x16 blocks, head_dim 64 / 128, at most 64 blocks.
 bool bwd_supported(int head_dim, int tile, int n_tiles, int dtype);

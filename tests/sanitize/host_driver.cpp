@@ -197,8 +197,8 @@ int main() {
     CHECK(ssba_forward_layers_ex(&d, layers, L, idx, lib, scr, lsb - 1, nullptr) == SSBA_ERR_WORKSPACE);
     CHECK(stub_calls().empty());
     CHECK(ssba_forward_layers_ex(&d, layers, L, idx, lib, scr, lsb, nullptr) == SSBA_OK);
-    // four layers ran: one pooling pre-pass over their keys, then each
-    // layer's gated attention
+    // four layers ran: one pooling launch over their keys, then one gated
+    // attention launch over the same layers
     CHECK(stub_calls().size() == 8);
     const int ran[] = {0, 1, 3, 4};
     const size_t pooled = (size_t)8 * 16 * 64 * 64;   // the pooled key sums follow 8 B H T_b D bytes of q sums
@@ -208,7 +208,9 @@ int main() {
       CHECK(std::strcmp(pre.what, "pool_keys_layers") == 0 && pre.index == layers[l].k);
       CHECK(pre.scratch == scr + (size_t)l * stride + pooled && pre.keep == (l & 1));
       const StubCall& att = stub_calls()[4 + i];
+      CHECK(std::strcmp(att.what, "attn_layers") == 0 && att.out == layers[l].o);
       CHECK(att.gated == 1 && att.keep == 3 + l);
+      CHECK(att.flags == scr + (size_t)l * stride + 2 * pooled);
       CHECK(att.index == idx + (size_t)l * (ib / 4));
       CHECK(att.scratch == pre.scratch);
       // offsets alternate sign: +4 on even layers, -4 (reduced: 60) on odd ones

@@ -42,6 +42,16 @@ hipError_t launch_gate_static(const IndexArgs& a, int, hipStream_t) { return rec
 hipError_t launch_attn_bf16(const AttnArgs& a, int, int, hipStream_t) { return rec_attn("attn_bf16", a); }
 hipError_t launch_attn_f32(const AttnArgs& a, int, int, hipStream_t) { return rec_attn("attn_f32", a); }
 hipError_t launch_attn_mfma(const AttnArgs& a, int, int, hipStream_t) { return rec_attn("attn_mfma", a); }
+// One record per layer, as rec_attn would make for that layer's own launch.
+hipError_t launch_attn_mfma_layers(const AttnLayers& p, int n_layers, int, hipStream_t) {
+  if (n_layers < 1 || n_layers > kAttnLayersMax) return hipErrorInvalidValue;
+  for (int i = 0; i < n_layers; ++i) {
+    const Frame& f = p.f[p.parity[i] & 1];
+    stub_calls().push_back({"attn_layers", p.index_out[i], p.kb[i], p.flags[i], p.o[i], p.keep[i], f.sy, f.sx,
+                            p.a.gated});
+  }
+  return hipSuccess;
+}
 hipError_t launch_backward(const BwdArgs& a, int, hipStream_t) {
   stub_calls().push_back({"backward", a.index, a.lse2, a.kmask, a.dq, 0, a.f.sy, a.f.sx, 0});
   return hipSuccess;
