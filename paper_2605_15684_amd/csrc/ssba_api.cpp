@@ -557,13 +557,65 @@ ssba_status ssba_forward_layers_ex(const ssba_desc* d, const ssba_layer* layers,
         ++np;
       }
       if (np > 0 && (ssba::launch_pool_keys_layers(p, np, hs) != hipSuccess ||
-                     ssba::launch_attn_mfma_layers(at, np, d->head_dim, hs) != hipSuccess))
+                     ssba::launch_attn_mfma_layers(at, np, d->head_dim, 8, hs) != hipSuccess))
         return SSBA_ERR_HIP;
       l0 = l1;
     }
     return SSBA_OK;
   }
   int cached[2] = {-1, -1};   // static gates: the layer whose index serves each parity
+  if (d->dtype == SSBA_DT_BF16 &&
+      ssba::mfma_supported(d->head_dim, d->tile, false, s.n_tiles, s.seq, (int64_t)s.seq * s.st)) {
+    // Each layer's index as one call per layer builds it (the head-shared
+    // top-k gate per layer, a static gate once per offset parity), then the
+    // attention of up to 32 layers in one launch (grid y = layer) reading
+    // those indices: the same bits as one call per layer.
+    ssba_desc odd = base;
+    odd.shift_y = -d->shift_y;
+    odd.shift_x = -d->shift_x;
+    Shape so;
+    st = check_desc(&odd, &so);
+    if (st != SSBA_OK) return st;
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    ssba::AttnLayers at;
+    for (int l0 = 0; l0 < n_layers;) {
+      std::memset(&at, 0, sizeof(at));
+      at.f[0] = s.f;
+      at.f[1] = so.f;
+      at.a = attn_args(&base, s, nullptr, nullptr, nullptr, nullptr, nullptr, false);
+      int np = 0, l1 = l0;
+      for (; l1 < n_layers && np < ssba::kAttnLayersMax; ++l1) {
+        const ssba_layer& L = layers[l1];
+        if (L.skip) continue;
+        ssba_desc dl = (l1 & 1) ? odd : base;
+        int32_t* il = index + (size_t)l1 * idx_elems;
+        void* sl = static_cast<char*>(scratch) + (size_t)l1 * scr_stride;
+        const int par = l1 & 1;
+        if (is_topk(d->gate)) {
+          dl.keep = L.keep;
+          st = ssba_build_index_ex(&dl, L.q, L.k, il, idx_bytes, sl, scr_stride, stream);
+          at.index[np] = il;
+        } else {
+          if (cached[par] < 0) {
+            st = ssba_build_index_ex(&dl, nullptr, nullptr, il, idx_bytes, sl, scr_stride, stream);
+            cached[par] = l1;
+          }
+          at.index[np] = index + (size_t)cached[par] * idx_elems;
+        }
+        if (st != SSBA_OK) return st;
+        at.q[np] = L.q;
+        at.k[np] = L.k;
+        at.v[np] = L.v;
+        at.o[np] = L.o;
+        at.parity[np] = par;
+        ++np;
+      }
+      if (np > 0 && ssba::launch_attn_mfma_layers(at, np, d->head_dim, d->tile, hs) != hipSuccess)
+        return SSBA_ERR_HIP;
+      l0 = l1;
+    }
+    return SSBA_OK;
+  }
   for (int l = 0; l < n_layers; ++l) {
     const ssba_layer& L = layers[l];
     if (L.skip) continue;

@@ -728,12 +728,12 @@ k_attn_mfma(AttnArgs a) {
   attn_mfma_body<D, TILE_LOG2, DENSE, GATED>(a);
 }
 
-// Gated attention of several layers in one launch (grid y = layer): the
+// Attention of several layers in one launch (grid y = layer): the
 // workgroups of layer l + 1 start as those of layer l finish, so one layer's
 // tail and the next one's start overlap.  Each workgroup runs exactly what
 // it runs in a one-layer launch.
-template <int D>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 64 ? 4 : 2)))
+template <int D, int TILE_LOG2, bool GATED>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 64 ? 4 : GATED ? 2 : 3)))
 k_attn_mfma_layers(AttnLayers p) {
   const int l = blockIdx.y;
   AttnArgs a = p.a;
@@ -741,12 +741,16 @@ k_attn_mfma_layers(AttnLayers p) {
   a.k = p.k[l];
   a.v = p.v[l];
   a.o = p.o[l];
-  a.kb = p.kb[l];
-  a.index_out = p.index_out[l];
-  a.flags = p.flags[l];
-  a.keep = p.keep[l];
+  if constexpr (GATED) {
+    a.kb = p.kb[l];
+    a.index_out = p.index_out[l];
+    a.flags = p.flags[l];
+    a.keep = p.keep[l];
+  } else {
+    a.index = p.index[l];
+  }
   a.f = p.f[p.parity[l] & 1];
-  attn_mfma_body<D, 3, false, true>(a);
+  attn_mfma_body<D, TILE_LOG2, false, GATED>(a);
 }
 
 // Image and text workgroup counts of a launch.
@@ -765,20 +769,28 @@ void set_groups(AttnArgs& a, int tile) {
 
 }  // namespace
 
-hipError_t launch_attn_mfma_layers(const AttnLayers& p0, int n_layers, int head_dim, hipStream_t s) {
-  if (n_layers < 1 || n_layers > kAttnLayersMax || !p0.a.gated || p0.a.dense || p0.a.f.tile_log2 != 3 ||
-      (head_dim != 64 && head_dim != 128))
+hipError_t launch_attn_mfma_layers(const AttnLayers& p0, int n_layers, int head_dim, int tile, hipStream_t s) {
+  const bool gated = p0.a.gated != 0;
+  if (n_layers < 1 || n_layers > kAttnLayersMax || p0.a.dense || (head_dim != 64 && head_dim != 128) ||
+      (tile != 8 && tile != 16) || (gated && tile != 8) || p0.a.f.tile_log2 != (tile == 8 ? 3 : 4))
     return hipErrorInvalidValue;
   AttnLayers p = p0;
-  set_groups(p.a, 8);
+  set_groups(p.a, tile);
   // Several layers never fit the CUs at once: the chunk-count priorities
   // stay off (they only pay when the whole grid is resident).
   p.a.equalize = 0;
   const int64_t per_layer = (int64_t)p.a.batch * p.a.heads * p.a.groups_per_bh;
   if (per_layer <= 0) return hipSuccess;
   const dim3 grid((unsigned)per_layer, (unsigned)n_layers), block(256);
-  if (head_dim == 64) hipLaunchKernelGGL((k_attn_mfma_layers<64>), grid, block, 0, s, p);
-  else hipLaunchKernelGGL((k_attn_mfma_layers<128>), grid, block, 0, s, p);
+  if (head_dim == 64) {
+    if (gated) hipLaunchKernelGGL((k_attn_mfma_layers<64, 3, true>), grid, block, 0, s, p);
+    else if (tile == 8) hipLaunchKernelGGL((k_attn_mfma_layers<64, 3, false>), grid, block, 0, s, p);
+    else hipLaunchKernelGGL((k_attn_mfma_layers<64, 4, false>), grid, block, 0, s, p);
+  } else {
+    if (gated) hipLaunchKernelGGL((k_attn_mfma_layers<128, 3, true>), grid, block, 0, s, p);
+    else if (tile == 8) hipLaunchKernelGGL((k_attn_mfma_layers<128, 3, false>), grid, block, 0, s, p);
+    else hipLaunchKernelGGL((k_attn_mfma_layers<128, 4, false>), grid, block, 0, s, p);
+  }
   return hipGetLastError();
 }
 

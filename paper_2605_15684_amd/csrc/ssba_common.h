@@ -100,9 +100,10 @@ struct AttnArgs {
   int equalize;
 };
 
-// Gated attention of up to kAttnLayersMax layers of one shape in one launch
-// (the layer driver): layer y reads q/k/v[y] and kb[y], writes o[y],
-// index_out[y] and flags[y], keeps keep[y] blocks, in frame f[parity[y]];
+// Attention of up to kAttnLayersMax layers of one shape in one launch (the
+// layer driver): layer y reads q/k/v[y] and writes o[y] in frame
+// f[parity[y]]; a gated launch (a.gated) reads kb[y], writes index_out[y]
+// and flags[y] and keeps keep[y] blocks, an ungated one reads index[y];
 // every other field is a's.
 constexpr int kAttnLayersMax = 32;
 struct AttnLayers {
@@ -112,6 +113,7 @@ struct AttnLayers {
   const void* k[kAttnLayersMax];
   const void* v[kAttnLayersMax];
   void* o[kAttnLayersMax];
+  const int32_t* index[kAttnLayersMax];
   const double* kb[kAttnLayersMax];
   int32_t* index_out[kAttnLayersMax];
   int32_t* flags[kAttnLayersMax];
@@ -183,8 +185,9 @@ hipError_t launch_attn_f32(const AttnArgs& a, int head_dim, int tile, hipStream_
 // gated launches (a.gated) need 8x8 blocks.
 bool mfma_supported(int head_dim, int tile, bool dense, int n_tiles, int seq, int64_t span);
 hipError_t launch_attn_mfma(const AttnArgs& a, int head_dim, int tile, hipStream_t s);
-// Gated attention (bf16, 8x8 blocks, D 64 or 128) of n_layers <= kAttnLayersMax layers.
-hipError_t launch_attn_mfma_layers(const AttnLayers& p, int n_layers, int head_dim, hipStream_t s);
+// Attention (bf16, D 64 or 128; 8x8 blocks when gated, 8x8 or 16x16 with an
+// index) of n_layers <= kAttnLayersMax layers, on shapes mfma_supported takes.
+hipError_t launch_attn_mfma_layers(const AttnLayers& p, int n_layers, int head_dim, int tile, hipStream_t s);
 const char* mfma_kernel_name(int head_dim, int tile, bool dense, bool gated);
 // Backward: bf16, 8x8 or 16x16 blocks, head_dim 64 / 128, at most 64 blocks.
 bool bwd_supported(int head_dim, int tile, int n_tiles, int dtype);

@@ -43,12 +43,14 @@ hipError_t launch_attn_bf16(const AttnArgs& a, int, int, hipStream_t) { return r
 hipError_t launch_attn_f32(const AttnArgs& a, int, int, hipStream_t) { return rec_attn("attn_f32", a); }
 hipError_t launch_attn_mfma(const AttnArgs& a, int, int, hipStream_t) { return rec_attn("attn_mfma", a); }
 // One record per layer, as rec_attn would make for that layer's own launch.
-hipError_t launch_attn_mfma_layers(const AttnLayers& p, int n_layers, int, hipStream_t) {
+hipError_t launch_attn_mfma_layers(const AttnLayers& p, int n_layers, int, int, hipStream_t) {
   if (n_layers < 1 || n_layers > kAttnLayersMax) return hipErrorInvalidValue;
   for (int i = 0; i < n_layers; ++i) {
     const Frame& f = p.f[p.parity[i] & 1];
-    stub_calls().push_back({"attn_layers", p.index_out[i], p.kb[i], p.flags[i], p.o[i], p.keep[i], f.sy, f.sx,
-                            p.a.gated});
+    if (p.a.gated)
+      stub_calls().push_back({"attn_layers", p.index_out[i], p.kb[i], p.flags[i], p.o[i], p.keep[i], f.sy, f.sx, 1});
+    else
+      stub_calls().push_back({"attn_layers", p.index[i], nullptr, nullptr, p.o[i], 0, f.sy, f.sx, 0});
   }
   return hipSuccess;
 }

@@ -433,6 +433,35 @@ def test_layer_stack_equals_per_layer_calls(gate, window):
             assert ssba.read_status(dl_status, scratch[l]) == 0
 
 
+@pytest.mark.parametrize("gate,window", [("window", (2, 2)), ("topk_shared", (1, 1))])
+def test_layer_stack_16x16_blocks_d128(gate, window):
+    """The layer driver's one attention launch over several layers with
+    16x16 blocks at head_dim 128 (the 128x128-grid kernels): every layer's
+    output equals one call per layer."""
+    from paper_2605_15684_amd import ssba
+    w = preset("grid64", heads=2, head_dim=128, tile=16, n_text=0, gate=gate, window=window, shift=(8, 8))
+    keeps = [5, 9, 3, 16]
+    skips = [False, True, False, False]
+    layers = _layer_stack(w, keeps, skips, seed0=50)
+    desc = gpu_desc(w, layers[0]["q"])
+    index, scratch = ssba.forward_layers(layers, desc)
+    torch.cuda.synchronize()
+    for l, L in enumerate(layers):
+        if L["skip"]:
+            assert bool((L["out"] == 7.0).all())
+            continue
+        wl = w.with_(shift=(8, 8) if l % 2 == 0 else (-8, -8), keep=keeps[l])
+        dl = gpu_desc(wl, L["q"])
+        if gate == "topk_shared":
+            idx1, _ = ssba.build_index(L["q"], L["k"], dl)
+            assert torch.equal(index[l], idx1), f"layer {l}"
+        else:
+            idx1, _ = ssba.build_index(None, None, dl)
+        out1 = ssba.forward(L["q"], L["k"], L["v"], idx1, dl)
+        torch.cuda.synchronize()
+        assert torch.equal(L["out"], out1), f"layer {l}"
+
+
 def test_layer_stack_beyond_one_prepass_launch():
     """A stack longer than one batched pooling launch takes (32 layers), with
     skipped layers and text tokens: every layer's index, status and output
