@@ -567,9 +567,11 @@ ssba_status ssba_forward_layers_ex(const ssba_desc* d, const ssba_layer* layers,
   if (d->dtype == SSBA_DT_BF16 &&
       ssba::mfma_supported(d->head_dim, d->tile, false, s.n_tiles, s.seq, (int64_t)s.seq * s.st)) {
     // Each layer's index as one call per layer builds it (the head-shared
-    // top-k gate per layer, a static gate once per offset parity), then the
-    // attention of up to 32 layers in one launch (grid y = layer) reading
-    // those indices: the same bits as one call per layer.
+    // top-k gate of up to 32 layers in one launch per step, a static gate
+    // once per offset parity), then the attention of those layers in one
+    // launch (grid y = layer) reading their indices: the same bits as one
+    // call per layer.
+    static_assert(ssba::kIndexLayersMax == ssba::kAttnLayersMax, "one chunk of layers per launch group");
     ssba_desc odd = base;
     odd.shift_y = -d->shift_y;
     odd.shift_x = -d->shift_x;
@@ -577,32 +579,44 @@ ssba_status ssba_forward_layers_ex(const ssba_desc* d, const ssba_layer* layers,
     st = check_desc(&odd, &so);
     if (st != SSBA_OK) return st;
     hipStream_t hs = static_cast<hipStream_t>(stream);
+    const bool shared = d->gate == SSBA_GATE_TOPK_SHARED;
     ssba::AttnLayers at;
+    ssba::IndexLayers ix;
     for (int l0 = 0; l0 < n_layers;) {
       std::memset(&at, 0, sizeof(at));
-      at.f[0] = s.f;
-      at.f[1] = so.f;
+      std::memset(&ix, 0, sizeof(ix));
+      at.f[0] = ix.f[0] = s.f;
+      at.f[1] = ix.f[1] = so.f;
       at.a = attn_args(&base, s, nullptr, nullptr, nullptr, nullptr, nullptr, false);
+      ix.a = index_args(&base, s, nullptr, nullptr, nullptr, scratch);
       int np = 0, l1 = l0;
       for (; l1 < n_layers && np < ssba::kAttnLayersMax; ++l1) {
         const ssba_layer& L = layers[l1];
         if (L.skip) continue;
-        ssba_desc dl = (l1 & 1) ? odd : base;
         int32_t* il = index + (size_t)l1 * idx_elems;
         void* sl = static_cast<char*>(scratch) + (size_t)l1 * scr_stride;
         const int par = l1 & 1;
-        if (is_topk(d->gate)) {
-          dl.keep = L.keep;
-          st = ssba_build_index_ex(&dl, L.q, L.k, il, idx_bytes, sl, scr_stride, stream);
+        if (shared) {
+          const IndexArgs ia = index_args(&base, s, L.q, L.k, il, sl);
+          ix.q[np] = L.q;
+          ix.k[np] = L.k;
+          ix.index[np] = il;
+          ix.qb[np] = ia.qb;
+          ix.kb[np] = ia.kb;
+          ix.flags[np] = ia.flags;
+          ix.srows[np] = ia.srows;
+          ix.keep[np] = L.keep;
+          ix.parity[np] = par;
           at.index[np] = il;
         } else {
           if (cached[par] < 0) {
+            const ssba_desc& dl = par ? odd : base;
             st = ssba_build_index_ex(&dl, nullptr, nullptr, il, idx_bytes, sl, scr_stride, stream);
+            if (st != SSBA_OK) return st;
             cached[par] = l1;
           }
           at.index[np] = index + (size_t)cached[par] * idx_elems;
         }
-        if (st != SSBA_OK) return st;
         at.q[np] = L.q;
         at.k[np] = L.k;
         at.v[np] = L.v;
@@ -610,7 +624,8 @@ ssba_status ssba_forward_layers_ex(const ssba_desc* d, const ssba_layer* layers,
         at.parity[np] = par;
         ++np;
       }
-      if (np > 0 && ssba::launch_attn_mfma_layers(at, np, d->head_dim, d->tile, hs) != hipSuccess)
+      if (np > 0 && ((shared && ssba::launch_topk_shared_layers(ix, np, hs) != hipSuccess) ||
+                     ssba::launch_attn_mfma_layers(at, np, d->head_dim, d->tile, hs) != hipSuccess))
         return SSBA_ERR_HIP;
       l0 = l1;
     }

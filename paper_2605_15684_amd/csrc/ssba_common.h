@@ -168,6 +168,26 @@ struct PoolLayers {
   int parity[kPoolLayersMax];
 };
 
+// The head-shared top-k gate of up to kIndexLayersMax layers of one shape,
+// each step one launch (the layer driver): layer y reads q/k[y], writes its
+// pooled sums to qb/kb[y], its per-head rows to srows[y], its index and
+// flags to index/flags[y], keeps keep[y] blocks, in frame f[parity[y]];
+// every other field is a's.
+constexpr int kIndexLayersMax = 32;
+struct IndexLayers {
+  IndexArgs a;
+  Frame f[2];
+  const void* q[kIndexLayersMax];
+  const void* k[kIndexLayersMax];
+  int32_t* index[kIndexLayersMax];
+  double* qb[kIndexLayersMax];
+  double* kb[kIndexLayersMax];
+  int32_t* flags[kIndexLayersMax];
+  double* srows[kIndexLayersMax];
+  int keep[kIndexLayersMax];
+  int parity[kIndexLayersMax];
+};
+
 // Launchers (each returns hipGetLastError() of its launch).
 hipError_t launch_pool(const IndexArgs& a, int dtype, hipStream_t s);
 // Pooled key sums only (bf16, 8x8 blocks): the pre-pass of the gated attention
@@ -176,6 +196,9 @@ hipError_t launch_pool_keys(const IndexArgs& a, hipStream_t s);
 // The same for n_layers <= kPoolLayersMax layers of one shape.
 hipError_t launch_pool_keys_layers(const PoolLayers& p, int n_layers, hipStream_t s);
 hipError_t launch_gate_topk(const IndexArgs& a, hipStream_t s);
+// The head-shared gate (bf16, 8x8 or 16x16 blocks, T_b <= 64) of
+// n_layers <= kIndexLayersMax layers: pooling, affinity rows, ranking.
+hipError_t launch_topk_shared_layers(const IndexLayers& p, int n_layers, hipStream_t s);
 // Head-shared top-k gate: per-head affinity rows, then their sum over heads.
 hipError_t launch_gate_topk_shared(const IndexArgs& a, hipStream_t s);
 hipError_t launch_gate_static(const IndexArgs& a, int gate, hipStream_t s);

@@ -205,7 +205,7 @@ __global__ void __launch_bounds__(MAXT) k_gate_topk(IndexArgs a) {
 // Head-shared gate, step 1: one workgroup per query block (i, h, b) writes
 // its row of the per-head affinity, S_h[i][j] for j < T_b, to srows.
 template <int D, int MAXT>
-__global__ void __launch_bounds__(MAXT) k_affinity_rows(IndexArgs a) {
+__device__ __forceinline__ void affinity_rows_body(const IndexArgs& a) {
   int i, h, b;
   unit_of(a, i, h, b);
   const int tb = a.n_tiles, j = threadIdx.x;
@@ -214,11 +214,16 @@ __global__ void __launch_bounds__(MAXT) k_affinity_rows(IndexArgs a) {
     a.srows[(bh * tb + i) * tb + j] = affinity_entry<D>(a.qb + (bh * tb + i) * D, a.kb + bh * D * tb + j, tb);
 }
 
+template <int D, int MAXT>
+__global__ void __launch_bounds__(MAXT) k_affinity_rows(IndexArgs a) {
+  affinity_rows_body<D, MAXT>(a);
+}
+
 // Head-shared gate, step 2: one workgroup per query block (i, b); thread j
 // adds S_h[i][j] over heads h = 0, 1, ..., H-1 in that order (fp64), ranks
 // the sums and writes the same kept list and status flag for every head.
 template <int MAXT>
-__global__ void __launch_bounds__(MAXT) k_gate_shared(IndexArgs a) {
+__device__ __forceinline__ void gate_shared_body(const IndexArgs& a) {
   extern __shared__ uint64_t keys[];   // [T_b]
   __shared__ int wave_kept[16];
   __shared__ int bad;
@@ -264,6 +269,42 @@ __global__ void __launch_bounds__(MAXT) k_gate_shared(IndexArgs a) {
       a.flags[bh * tb + i] = bad;
     }
   }
+}
+
+template <int MAXT>
+__global__ void __launch_bounds__(MAXT) k_gate_shared(IndexArgs a) {
+  gate_shared_body<MAXT>(a);
+}
+
+// The head-shared gate of several layers of one shape, one launch per step
+// (grid y = layer): each workgroup does what it does for its own layer.
+__device__ __forceinline__ IndexArgs layer_index_args(const IndexLayers& p) {
+  const int l = blockIdx.y;
+  IndexArgs a = p.a;
+  a.q = p.q[l];
+  a.k = p.k[l];
+  a.index = p.index[l];
+  a.qb = p.qb[l];
+  a.kb = p.kb[l];
+  a.flags = p.flags[l];
+  a.srows = p.srows[l];
+  a.keep = p.keep[l];
+  a.f = p.f[p.parity[l] & 1];
+  return a;
+}
+
+template <int TILE_LOG2, int D>
+__global__ void __launch_bounds__(256) k_pool_layers(IndexLayers p) {
+  pool_block<SSBA_DT_BF16, TILE_LOG2, D, 2>(layer_index_args(p));
+}
+
+template <int D>
+__global__ void __launch_bounds__(64) k_affinity_rows_layers(IndexLayers p) {
+  affinity_rows_body<D, 64>(layer_index_args(p));
+}
+
+__global__ void __launch_bounds__(64) k_gate_shared_layers(IndexLayers p) {
+  gate_shared_body<64>(layer_index_args(p));
 }
 
 // Window (win_h x win_w blocks of the shifted frame) and dense gates.
@@ -374,6 +415,28 @@ hipError_t launch_gate_topk_shared(const IndexArgs& a, hipStream_t s) {
     else hipLaunchKernelGGL((k_affinity_rows<128, 1024>), grid_rows, block, 0, s, a);
     hipLaunchKernelGGL((k_gate_shared<1024>), grid_b, block, lds, s, a);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_topk_shared_layers(const IndexLayers& p, int n_layers, hipStream_t s) {
+  const IndexArgs& a = p.a;
+  const int tl = a.f.tile_log2;
+  if (n_layers < 1 || n_layers > kIndexLayersMax || a.n_tiles < 1 || a.n_tiles > 64 || (tl != 3 && tl != 4) ||
+      p.f[0].tile_log2 != tl || p.f[1].tile_log2 != tl || (a.head_dim != 64 && a.head_dim != 128))
+    return hipErrorInvalidValue;
+  const dim3 grid_rows(a.n_tiles * a.heads * a.batch, n_layers), grid_b(a.n_tiles * a.batch, n_layers);
+  const dim3 block_pool(256), block(round_threads(a.n_tiles));
+  const size_t lds = sizeof(uint64_t) * (size_t)a.n_tiles;
+  if (a.head_dim == 64) {
+    if (tl == 3) hipLaunchKernelGGL((k_pool_layers<3, 64>), grid_rows, block_pool, 0, s, p);
+    else hipLaunchKernelGGL((k_pool_layers<4, 64>), grid_rows, block_pool, 0, s, p);
+    hipLaunchKernelGGL((k_affinity_rows_layers<64>), grid_rows, block, 0, s, p);
+  } else {
+    if (tl == 3) hipLaunchKernelGGL((k_pool_layers<3, 128>), grid_rows, block_pool, 0, s, p);
+    else hipLaunchKernelGGL((k_pool_layers<4, 128>), grid_rows, block_pool, 0, s, p);
+    hipLaunchKernelGGL((k_affinity_rows_layers<128>), grid_rows, block, 0, s, p);
+  }
+  hipLaunchKernelGGL(k_gate_shared_layers, grid_b, block, lds, s, p);
   return hipGetLastError();
 }
 

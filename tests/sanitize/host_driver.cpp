@@ -263,26 +263,31 @@ int main() {
       }
     }
     CHECK(gates == 2 && attn == 4);
-    // head-shared top-k gate: each running layer builds its own index (pool
-    // and gate), then one attention launch reads every layer's slice
+    // head-shared top-k gate: one launch group builds every running layer's
+    // index in its own slice, then one attention launch reads them
     ssba_desc sh = d;
     sh.gate = SSBA_GATE_TOPK_SHARED;
     size_t sib = 0, ssb = 0;
     CHECK(ssba_layers_workspace_size(&sh, L, &sib, &ssb) == SSBA_OK);
     Buffers bs(tensor, sib, ssb);
     int32_t* sidx = reinterpret_cast<int32_t*>(bs.index.data());
+    char* sscr = reinterpret_cast<char*>(bs.scratch.data());
     stub_calls().clear();
-    CHECK(ssba_forward_layers_ex(&sh, layers, L, sidx, sib, bs.scratch.data(), ssb, nullptr) == SSBA_OK);
-    CHECK(stub_calls().size() == 12);
+    CHECK(ssba_forward_layers_ex(&sh, layers, L, sidx, sib, sscr, ssb, nullptr) == SSBA_OK);
+    CHECK(stub_calls().size() == 8);
+    const size_t sstride = ssb / L;
     for (int i = 0; i < 4; ++i) {
       const int l = ran[i];
-      CHECK(std::strcmp(stub_calls()[2 * i].what, "pool") == 0);
-      CHECK(std::strcmp(stub_calls()[2 * i + 1].what, "gate_shared") == 0);
-      CHECK(stub_calls()[2 * i + 1].index == sidx + (size_t)l * (sib / L / 4) && stub_calls()[2 * i + 1].keep == 3 + l);
-      const StubCall& att = stub_calls()[8 + i];
+      const StubCall& g = stub_calls()[i];
+      CHECK(std::strcmp(g.what, "shared_layers") == 0 && g.keep == 3 + l);
+      CHECK(g.index == sidx + (size_t)l * (sib / L / 4) && g.scratch == sscr + (size_t)l * sstride);
+      // q sums, k sums, then the per-head rows (8 B H T_b T_b), then the flags
+      CHECK(g.out == sscr + (size_t)l * sstride + 2 * pooled);
+      CHECK(g.flags == sscr + (size_t)l * sstride + 2 * pooled + (size_t)8 * 16 * 64 * 64);
+      CHECK(g.sy == ((l & 1) ? 60 : 4));
+      const StubCall& att = stub_calls()[4 + i];
       CHECK(std::strcmp(att.what, "attn_layers") == 0 && att.gated == 0);
-      CHECK(att.index == stub_calls()[2 * i + 1].index && att.out == layers[l].o);
-      CHECK(att.sy == ((l & 1) ? 60 : 4));
+      CHECK(att.index == g.index && att.out == layers[l].o && att.sy == g.sy);
     }
   }
 

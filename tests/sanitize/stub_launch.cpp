@@ -39,6 +39,15 @@ hipError_t launch_pool_keys_layers(const PoolLayers& p, int n_layers, hipStream_
 hipError_t launch_gate_topk(const IndexArgs& a, hipStream_t) { return rec_index("gate_topk", a); }
 hipError_t launch_gate_topk_shared(const IndexArgs& a, hipStream_t) { return rec_index("gate_shared", a); }
 hipError_t launch_gate_static(const IndexArgs& a, int, hipStream_t) { return rec_index("gate_static", a); }
+// One record per layer: its index, pooled sums, flags, keep and frame offsets.
+hipError_t launch_topk_shared_layers(const IndexLayers& p, int n_layers, hipStream_t) {
+  if (n_layers < 1 || n_layers > kIndexLayersMax) return hipErrorInvalidValue;
+  for (int i = 0; i < n_layers; ++i) {
+    const Frame& f = p.f[p.parity[i] & 1];
+    stub_calls().push_back({"shared_layers", p.index[i], p.qb[i], p.flags[i], p.srows[i], p.keep[i], f.sy, f.sx, 0});
+  }
+  return hipSuccess;
+}
 hipError_t launch_attn_bf16(const AttnArgs& a, int, int, hipStream_t) { return rec_attn("attn_bf16", a); }
 hipError_t launch_attn_f32(const AttnArgs& a, int, int, hipStream_t) { return rec_attn("attn_f32", a); }
 hipError_t launch_attn_mfma(const AttnArgs& a, int, int, hipStream_t) { return rec_attn("attn_mfma", a); }
