@@ -462,6 +462,30 @@ def test_layer_stack_16x16_blocks_d128(gate, window):
         assert torch.equal(L["out"], out1), f"layer {l}"
 
 
+def test_layer_stack_topk_d128():
+    """The batched pooling and gated attention launches at head_dim 128
+    (8x8 blocks, text tokens): every layer equals one fused call."""
+    from paper_2605_15684_amd import ssba
+    w = preset("grid64", heads=2, head_dim=128, grid_h=32, grid_w=48, n_text=20, shift=(4, 4))
+    keeps = [3, 11, 24, 1]
+    skips = [False, False, True, False]
+    layers = _layer_stack(w, keeps, skips, seed0=70)
+    desc = gpu_desc(w, layers[0]["q"])
+    index, scratch = ssba.forward_layers(layers, desc)
+    torch.cuda.synchronize()
+    for l, L in enumerate(layers):
+        if L["skip"]:
+            assert bool((L["out"] == 7.0).all())
+            continue
+        wl = w.with_(shift=(4, 4) if l % 2 == 0 else (-4, -4), keep=keeps[l])
+        dl = gpu_desc(wl, L["q"])
+        idx1, _, out1 = ssba.forward_topk(L["q"], L["k"], L["v"], dl)
+        torch.cuda.synchronize()
+        assert torch.equal(index[l], idx1), f"layer {l}"
+        assert torch.equal(L["out"], out1), f"layer {l}"
+        assert ssba.read_status(dl, scratch[l]) == 0
+
+
 def test_layer_stack_beyond_one_prepass_launch():
     """A stack longer than one batched pooling launch takes (32 layers), with
     skipped layers and text tokens: every layer's index, status and output
