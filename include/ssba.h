@@ -289,12 +289,15 @@ ssba_status ssba_layers_workspace_size(const ssba_desc* d, int n_layers, size_t*
  * Static gates depend only on the frame, so the index is built once per
  * offset parity (in the slice of the first layer of that parity that runs)
  * and reused by the later layers of that parity, whose slices are left
- * untouched.  Where ssba_forward_topk gates inside the attention kernel
- * (bf16, 8x8 blocks), the key pooling of up to 32 running layers goes into
- * one launch ahead of their attention launches (same arithmetic, same
- * slices, so the same bits as one call per layer).  Every layer is checked
- * before anything is launched; a HIP launch failure stops the stack after
- * the layers already enqueued. */
+ * untouched.  Where the attention runs on the matrix-core kernels (bf16,
+ * D 64/128, 8x8 or 16x16 blocks, T_b <= 64), up to 32 running layers share
+ * each launch: for the top-k gate one launch pools their keys and one runs
+ * their gated attention; for the head-shared gate one launch per gate step
+ * builds their indices; then (for it and the static gates) one launch runs
+ * their attention.  Each workgroup computes what it computes in a one-layer
+ * launch, so the results are the same bits as one call per layer.  Every
+ * layer is checked before anything is launched; a HIP launch failure stops
+ * the stack after the layers already enqueued. */
 ssba_status ssba_forward_layers(const ssba_desc* d, const ssba_layer* layers, int n_layers,
                                 int32_t* index, void* scratch, void* hip_stream);
 
