@@ -28,6 +28,9 @@ Steps, in the paper's order and notation:
                (Section 2.1.2, Sparse-Depth Pruning).
   mask      -- expand G to token resolution, pad text rows and columns with
                ones (Section 2.2.1; Algorithm 1, expand and pad steps).
+  rope      -- the rotary position embedding of the image queries and keys
+               that Algorithm 1 applies first (2-D axial reading, fp64,
+               rounded to bf16).
   attention -- masked softmax attention over [text; image] in fp64
                (Algorithm 1, attention step).
   backward  -- gradients of the attention with respect to Q, K and V with the
@@ -37,7 +40,9 @@ Steps, in the paper's order and notation:
 Readings where the paper is silent (each also listed in the design notes):
 k counts dropped blocks per query row; sums rather than means are ranked; ties
 keep the lower index; text queries attend densely; wrapped blocks get no extra
-mask; the softmax scale is 1/sqrt(head_dim).
+mask; the softmax scale is 1/sqrt(head_dim); the rotary embedding is the 2-D
+axial form (row in the first half of the channels, column in the second,
+frequency base 10000), computed in fp64 and rounded to bf16.
 
 Pins: every function here is checked against independent facts in
 tests/test_oracle_*.py (brute-force enumeration, library routines on special
@@ -277,6 +282,66 @@ def ssba(q, k, v, *, grid_h, grid_w, tile, shift=(0, 0), n_text=0, gate="topk", 
     o = attention(q64, k64, v64, idx, grid_h=grid_h, grid_w=grid_w, tile=tile, shift=shift,
                   n_text=n_text, scale=scale)
     return idx, o
+
+
+# --------------------------------------------------------------------------
+# Rotary position embedding of the image queries and keys (Algorithm 1,
+# first step), applied before pooling.  The paper names the step but not the
+# variant; the reading (listed in the design notes) is the 2-D axial form:
+# channels [0, D/2) rotate with the token's row y, channels [D/2, D) with its
+# column x (positions in the unshifted image grid); inside a half, pair i is
+# channels (2i, 2i + 1) of that half, turned by the angle
+# pos * theta**(-i / (D/4)).  Text tokens are not rotated.  The rotation runs
+# in fp64 with every product rounded once (no fused multiply-add) and the
+# results are rounded to bf16 (round to nearest even), the precision the
+# attention then reads.
+# --------------------------------------------------------------------------
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """Round fp64 values to the nearest bf16 value (8 significant bits,
+    ties to even), directly from fp64 (no intermediate fp32 rounding)."""
+    x = np.asarray(x, np.float64)
+    m, e = np.frexp(x)                        # x = m * 2**e, 0.5 <= |m| < 1
+    return np.ldexp(np.rint(m * 256.0) / 256.0, e)   # np.rint rounds half to even
+
+
+def rope_angles(pos: np.ndarray, n_pairs: int, theta: float) -> np.ndarray:
+    """Angles [len(pos), n_pairs]: pos * theta**(-i / n_pairs), fp64."""
+    inv = np.array([theta ** (-i / n_pairs) for i in range(n_pairs)], np.float64)
+    return np.asarray(pos, np.float64)[:, None] * inv[None, :]
+
+
+def rope_2d(x: np.ndarray, *, grid_h: int, grid_w: int, n_text: int = 0,
+            theta: float = 10000.0) -> np.ndarray:
+    """The rotated copy of x [..., T, D] (fp64, not rounded; text rows and
+    every channel of them unchanged)."""
+    x = np.asarray(x, np.float64)
+    d = x.shape[-1]
+    if d % 4:
+        raise ValueError("head_dim must be a multiple of 4")
+    half, n_pairs = d // 2, d // 4
+    ids = np.arange(grid_h * grid_w)
+    out = x.copy()
+    for axis_pos, c0 in ((ids // grid_w, 0), (ids % grid_w, half)):
+        ang = rope_angles(axis_pos, n_pairs, theta)             # [T_img, n_pairs]
+        cos, sin = np.cos(ang), np.sin(ang)
+        a = x[..., n_text:, c0:c0 + half:2]                     # even channels of the half
+        b = x[..., n_text:, c0 + 1:c0 + half:2]                 # odd channels
+        out[..., n_text:, c0:c0 + half:2] = a * cos - b * sin
+        out[..., n_text:, c0 + 1:c0 + half:2] = a * sin + b * cos
+    return out
+
+
+def ssba_rope(q, k, v, *, grid_h, grid_w, tile, shift=(0, 0), n_text=0, gate="topk", keep=0,
+              window=(1, 1), scale=None, theta=10000.0):
+    """One SSBA call with the rotary step first: the rotated Q and K
+    (rounded to bf16), then index and output on them.  Returns
+    (q_rope, k_rope, index, out)."""
+    kw = dict(grid_h=grid_h, grid_w=grid_w, n_text=n_text, theta=theta)
+    qr = round_bf16(rope_2d(q, **kw))
+    kr = round_bf16(rope_2d(k, **kw))
+    idx, o = ssba(qr, kr, v, grid_h=grid_h, grid_w=grid_w, tile=tile, shift=shift, n_text=n_text,
+                  gate=gate, keep=keep, window=window, scale=scale)
+    return qr, kr, idx, o
 
 
 def layer_shift(layer: int, tile: int):
