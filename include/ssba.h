@@ -240,6 +240,29 @@ ssba_status ssba_backward_ex(const ssba_desc* d, const void* q, const void* k, c
                              void* dq, void* dk, void* dv, void* scratch, size_t scratch_bytes,
                              void* hip_stream);
 
+/* The rotary step of Algorithm 1 fused into the pooling pre-pass (bf16, 8x8
+ * blocks, D 64 or 128, at most 64 blocks; else SSBA_ERR_UNSUPPORTED): writes
+ * the rotated Q and K to q_rope and k_rope (layout of the descriptor; text
+ * rows copied unchanged) and the pooled sums of the rotated keys to scratch,
+ * as ssba_pool_keys_ex does for k.  The rotation (the paper names the step,
+ * not its variant) is the 2-D axial one: channels [0, D/2) turn with the
+ * token's row in the image grid, [D/2, D) with its column; pair i of a half
+ * (channels 2i, 2i+1) by the angle pos * theta^(-i / (D/4)), computed in
+ * fp64 and rounded to bf16 (nearest even).  theta <= 0 selects 10000; a
+ * non-finite theta is SSBA_ERR_ARG.  q_rope and k_rope may be q and k (in
+ * place) and must not otherwise overlap an input.  Sizes and errors as
+ * ssba_pool_keys_ex. */
+ssba_status ssba_rope_pool_keys_ex(const ssba_desc* d, const void* q, const void* k, void* q_rope, void* k_rope,
+                                  float theta, void* scratch, size_t scratch_bytes, void* hip_stream);
+
+/* ssba_forward_topk with the rotary step first (Algorithm 1 in full): the
+ * pre-pass above, then the gated attention on the rotated Q and K.  Writes
+ * q_rope, k_rope, the index and O; the results equal ssba_forward_topk on
+ * q_rope and k_rope.  Shapes, sizes and errors as ssba_forward_gated_ex. */
+ssba_status ssba_forward_topk_rope_ex(const ssba_desc* d, const void* q, const void* k, const void* v,
+                                     void* q_rope, void* k_rope, float theta, int32_t* index, size_t index_bytes,
+                                     void* scratch, size_t scratch_bytes, void* o, void* hip_stream);
+
 /* Largest scratch (bytes) that ssba_forward_topk_noalloc provides: the
  * fixed device array it uses in place of a caller buffer. */
 #define SSBA_NOALLOC_SCRATCH_BYTES ((size_t)8 << 20)

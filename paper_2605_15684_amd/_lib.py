@@ -34,7 +34,7 @@ EXPORTS = ("ssba_abi_version", "ssba_status_str", "ssba_workspace_size", "ssba_b
            "ssba_probe_mfma", "ssba_build_index_ex", "ssba_forward_ex", "ssba_forward_topk_ex",
            "ssba_forward_train_ex", "ssba_backward_ex", "ssba_forward_layers_ex",
            "ssba_read_device_status_ex", "ssba_forward_topk_noalloc", "ssba_pool_keys_ex",
-           "ssba_forward_gated_ex")
+           "ssba_forward_gated_ex", "ssba_rope_pool_keys_ex", "ssba_forward_topk_rope_ex")
 
 # Byte count that the binding passes for a buffer it cannot size (None).
 UNSIZED = ctypes.c_size_t(-1).value
@@ -138,7 +138,10 @@ def load(path: str = None) -> ctypes.CDLL:
                        ("ssba_read_device_status_ex", [dp, vp, sz, ctypes.POINTER(ctypes.c_int), vp]),
                        ("ssba_forward_topk_noalloc", [dp, vp, vp, vp, vp, sz, vp, vp]),
                        ("ssba_pool_keys_ex", [dp, vp, vp, sz, vp]),
-                       ("ssba_forward_gated_ex", [dp, vp, vp, vp, vp, sz, vp, sz, vp, vp])):
+                       ("ssba_forward_gated_ex", [dp, vp, vp, vp, vp, sz, vp, sz, vp, vp]),
+                       ("ssba_rope_pool_keys_ex", [dp, vp, vp, vp, vp, ctypes.c_float, vp, sz, vp]),
+                       ("ssba_forward_topk_rope_ex", [dp, vp, vp, vp, vp, vp, ctypes.c_float, vp, sz, vp, sz,
+                                                      vp, vp])):
         fn = getattr(lib, name)
         fn.restype = ctypes.c_int
         fn.argtypes = args
@@ -205,6 +208,21 @@ def forward_gated(desc, q_ptr, k_ptr, v_ptr, index_ptr, scratch_ptr, o_ptr, stre
     """ssba_forward_gated_ex: the gated attention launch of the fused top-k form."""
     return load().ssba_forward_gated_ex(ctypes.byref(desc), q_ptr, k_ptr, v_ptr, index_ptr, _nb(index_bytes),
                                         scratch_ptr, _nb(scratch_bytes), o_ptr, stream)
+
+
+def rope_pool_keys(desc, q_ptr, k_ptr, q_rope_ptr, k_rope_ptr, theta, scratch_ptr, stream,
+                   scratch_bytes=None) -> int:
+    """ssba_rope_pool_keys_ex: the rotary pre-pass of the fused call."""
+    return load().ssba_rope_pool_keys_ex(ctypes.byref(desc), q_ptr, k_ptr, q_rope_ptr, k_rope_ptr,
+                                         ctypes.c_float(theta), scratch_ptr, _nb(scratch_bytes), stream)
+
+
+def forward_topk_rope(desc, q_ptr, k_ptr, v_ptr, q_rope_ptr, k_rope_ptr, theta, index_ptr, scratch_ptr, o_ptr,
+                      stream, index_bytes=None, scratch_bytes=None) -> int:
+    """ssba_forward_topk_rope_ex: the rotary pre-pass, then the gated attention."""
+    return load().ssba_forward_topk_rope_ex(ctypes.byref(desc), q_ptr, k_ptr, v_ptr, q_rope_ptr, k_rope_ptr,
+                                            ctypes.c_float(theta), index_ptr, _nb(index_bytes), scratch_ptr,
+                                            _nb(scratch_bytes), o_ptr, stream)
 
 
 NOALLOC_SCRATCH_BYTES = 8 << 20   # SSBA_NOALLOC_SCRATCH_BYTES

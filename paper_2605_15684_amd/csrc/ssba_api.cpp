@@ -373,6 +373,38 @@ ssba_status ssba_forward_topk_ex(const ssba_desc* d, const void* q, const void* 
   return st != SSBA_OK ? st : ssba_forward_gated_ex(d, q, k, v, index, index_bytes, scratch, scratch_bytes, o, stream);
 }
 
+ssba_status ssba_rope_pool_keys_ex(const ssba_desc* d, const void* q, const void* k, void* q_rope, void* k_rope,
+                                  float theta, void* scratch, size_t scratch_bytes, void* stream) {
+  Shape s;
+  const ssba_status st = check_fused(d, &s, nullptr, k, nullptr, nullptr, 0, scratch, scratch_bytes, nullptr,
+                                     false);
+  if (st != SSBA_OK) return st;
+  if (!q || !q_rope || !k_rope || !aligned(q, 16) || !aligned(q_rope, 16) || !aligned(k_rope, 16))
+    return SSBA_ERR_ARG;
+  if (!std::isfinite(theta)) return SSBA_ERR_ARG;
+  const double base = theta > 0.f ? (double)theta : 10000.0;   // <= 0: the default base
+  ssba::RopeArgs r;
+  std::memset(&r, 0, sizeof(r));
+  r.a = index_args(d, s, q, k, nullptr, scratch);
+  r.q_out = q_rope;
+  r.k_out = k_rope;
+  const int pairs = d->head_dim / 4;
+  for (int i = 0; i < pairs; ++i) r.inv_freq[i] = std::pow(base, -(double)i / (double)pairs);
+  r.n_text_groups = (d->n_text + 63) / 64;
+  return ssba::launch_rope_pool_keys(r, static_cast<hipStream_t>(stream)) == hipSuccess ? SSBA_OK : SSBA_ERR_HIP;
+}
+
+ssba_status ssba_forward_topk_rope_ex(const ssba_desc* d, const void* q, const void* k, const void* v,
+                                     void* q_rope, void* k_rope, float theta, int32_t* index, size_t index_bytes,
+                                     void* scratch, size_t scratch_bytes, void* o, void* stream) {
+  Shape s;
+  const ssba_status st = check_fused(d, &s, q, k, v, index, index_bytes, scratch, scratch_bytes, o, true);
+  if (st != SSBA_OK) return st;
+  const ssba_status sr = ssba_rope_pool_keys_ex(d, q, k, q_rope, k_rope, theta, scratch, scratch_bytes, stream);
+  if (sr != SSBA_OK) return sr;
+  return ssba_forward_gated_ex(d, q_rope, k_rope, v, index, index_bytes, scratch, scratch_bytes, o, stream);
+}
+
 ssba_status ssba_forward_topk(const ssba_desc* d, const void* q, const void* k, const void* v,
                               int32_t* index, void* scratch, void* o, void* stream) {
   return ssba_forward_topk_ex(d, q, k, v, index, kUnchecked, scratch, kUnchecked, o, stream);

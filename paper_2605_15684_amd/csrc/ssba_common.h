@@ -168,6 +168,18 @@ struct PoolLayers {
   int parity[kPoolLayersMax];
 };
 
+// The rotary pre-pass of the fused call (bf16, 8x8 blocks): rotated Q and K
+// written to q_out / k_out and the pooled sums of the rotated keys to a.kb.
+// inv_freq[i] = theta^(-i / (D/4)) for the D/4 pairs of a half.
+struct RopeArgs {
+  IndexArgs a;
+  void* q_out;
+  void* k_out;
+  double inv_freq[32];
+  int n_text_groups;   // workgroups per (batch, head) that copy text rows
+};
+hipError_t launch_rope_pool_keys(const RopeArgs& r, hipStream_t s);
+
 // The head-shared top-k gate of up to kIndexLayersMax layers of one shape,
 // each step one launch (the layer driver): layer y reads q/k[y], writes its
 // pooled sums to qb/kb[y], its per-head rows to srows[y], its index and

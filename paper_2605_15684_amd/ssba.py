@@ -21,7 +21,8 @@ from . import _lib
 _lib.load()   # fail loudly at import if the HIP library is missing
 
 __all__ = ["make_desc", "desc_for", "alloc_workspace", "build_index", "forward", "forward_dense",
-           "forward_topk", "forward_layers", "forward_train", "backward", "attention", "read_status",
+           "forward_topk", "forward_topk_rope", "rope_pool_keys", "forward_layers", "forward_train", "backward",
+           "attention", "read_status",
            "layer_shift",
            "keep_from_rho", "SsbaError"]
 
@@ -197,6 +198,47 @@ def forward_gated(q, k, v, desc, index, scratch, out):
                                   scratch.data_ptr(), out.data_ptr(), _stream(q.device), _nbytes(index),
                                   _nbytes(scratch)), "ssba_forward_gated")
     return index, scratch, out
+
+
+def _rope_outputs(q, k, q_rope, k_rope):
+    mk = lambda t, like: torch.empty_strided(like.shape, like.stride(), dtype=like.dtype, device=like.device) \
+        if t is None else t
+    return mk(q_rope, q), mk(k_rope, k)
+
+
+def rope_pool_keys(q, k, desc, scratch, q_rope=None, k_rope=None, theta=10000.0):
+    """The rotary pre-pass alone (ssba_rope_pool_keys_ex): the rotated Q and
+    K (2-D axial rotary embedding of the image rows, Algorithm 1's first
+    step) and the pooled sums of the rotated keys in `scratch`.  Returns
+    (q_rope, k_rope)."""
+    q_rope, k_rope = _rope_outputs(q, k, q_rope, k_rope)
+    _check_tensors(desc, q, k, q_rope, k_rope)
+    _check_buffer(scratch, "scratch")
+    _lib.check(_lib.rope_pool_keys(desc, q.data_ptr(), k.data_ptr(), q_rope.data_ptr(), k_rope.data_ptr(),
+                                   float(theta), scratch.data_ptr(), _stream(q.device), _nbytes(scratch)),
+               "ssba_rope_pool_keys")
+    return q_rope, k_rope
+
+
+def forward_topk_rope(q, k, v, desc, theta=10000.0, q_rope=None, k_rope=None, index=None, scratch=None,
+                      out=None):
+    """Algorithm 1 in one call (ssba_forward_topk_rope_ex): rotary step,
+    pooling, gate and attention.  Returns (q_rope, k_rope, index, scratch,
+    out); the results equal forward_topk on (q_rope, k_rope, v)."""
+    q_rope, k_rope = _rope_outputs(q, k, q_rope, k_rope)
+    if out is None:
+        out = torch.empty_strided(q.shape, q.stride(), dtype=q.dtype, device=q.device)
+    _check_tensors(desc, q, k, v, out, q_rope, k_rope)
+    ib, sb = alloc_workspace(desc, q.device) if index is None or scratch is None else (index, scratch)
+    index = ib if index is None else index
+    scratch = sb if scratch is None else scratch
+    _check_buffer(index, "index", torch.int32)
+    _check_buffer(scratch, "scratch")
+    _lib.check(_lib.forward_topk_rope(desc, q.data_ptr(), k.data_ptr(), v.data_ptr(), q_rope.data_ptr(),
+                                      k_rope.data_ptr(), float(theta), index.data_ptr(), scratch.data_ptr(),
+                                      out.data_ptr(), _stream(q.device), _nbytes(index), _nbytes(scratch)),
+               "ssba_forward_topk_rope")
+    return q_rope, k_rope, index, scratch, out
 
 
 def forward_layers(layers, desc, index=None, scratch=None):

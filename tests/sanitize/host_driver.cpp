@@ -6,6 +6,7 @@
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
+#include <limits>
 #include <vector>
 
 #include "ssba.h"
@@ -140,6 +141,28 @@ int main() {
     CHECK(stub_calls().size() == 2 && std::strcmp(stub_calls()[0].what, "pool_keys") == 0);
     CHECK(stub_calls()[1].gated == 1 && stub_calls()[1].index == idx &&
           stub_calls()[1].scratch == static_cast<char*>(scr) + (size_t)8 * 16 * 64 * 64);
+
+    // the rotary form: pre-pass, then the gated attention on the rotated Q and K
+    {
+      Buffers rb(tensor, 0, 0);
+      stub_calls().clear();
+      CHECK(ssba_forward_topk_rope_ex(&d, b.q.data(), b.k.data(), b.v.data(), rb.q.data(), rb.k.data(), 0.f, idx,
+                                      ib, scr, sb - 1, b.o.data(), nullptr) == SSBA_ERR_WORKSPACE);
+      const float nan = std::numeric_limits<float>::quiet_NaN();
+      CHECK(ssba_forward_topk_rope_ex(&d, b.q.data(), b.k.data(), b.v.data(), rb.q.data(), rb.k.data(), nan, idx,
+                                      ib, scr, sb, b.o.data(), nullptr) == SSBA_ERR_ARG);
+      CHECK(ssba_rope_pool_keys_ex(&d, b.q.data(), b.k.data(), nullptr, rb.k.data(), 0.f, scr, sb, nullptr) ==
+            SSBA_ERR_ARG);
+      CHECK(stub_calls().empty());
+      CHECK(ssba_forward_topk_rope_ex(&d, b.q.data(), b.k.data(), b.v.data(), rb.q.data(), rb.k.data(), 0.f, idx,
+                                      ib, scr, sb, b.o.data(), nullptr) == SSBA_OK);
+      CHECK(stub_calls().size() == 2 && std::strcmp(stub_calls()[0].what, "rope") == 0);
+      CHECK(stub_calls()[0].out == rb.q.data() && stub_calls()[0].index == rb.k.data());
+      CHECK(stub_calls()[0].scratch == static_cast<char*>(scr) + (size_t)8 * 16 * 64 * 64);
+      CHECK(stub_calls()[0].keep == 1 && stub_calls()[0].gated == 0);   // inv_freq[0] = 1, no text rows
+      CHECK(stub_calls()[1].gated == 1 && stub_calls()[1].index == idx &&
+            stub_calls()[1].scratch == stub_calls()[0].scratch);
+    }
 
     // misaligned and missing pointers
     CHECK(ssba_forward_ex(&d, static_cast<char*>(static_cast<void*>(b.q.data())) + 2, b.k.data(), b.v.data(), idx,

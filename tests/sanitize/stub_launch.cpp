@@ -27,6 +27,13 @@ hipError_t rec_attn(const char* what, const AttnArgs& a) {
 
 hipError_t launch_pool(const IndexArgs& a, int, hipStream_t) { return rec_index("pool", a); }
 hipError_t launch_pool_keys(const IndexArgs& a, hipStream_t) { return rec_index("pool_keys", a); }
+// The rotary pre-pass: its pooled-key sums, rotated Q (in `out`) and the
+// first inverse frequency's bits in `keep` (inv_freq[0] is 1).
+hipError_t launch_rope_pool_keys(const RopeArgs& r, hipStream_t) {
+  stub_calls().push_back({"rope", r.k_out, r.a.kb, nullptr, r.q_out, (int)r.inv_freq[0], r.a.f.sy, r.a.f.sx,
+                          r.n_text_groups});
+  return hipSuccess;
+}
 // One record per layer: its pooled-key slice, parity (in keep) and frame offsets.
 hipError_t launch_pool_keys_layers(const PoolLayers& p, int n_layers, hipStream_t) {
   if (n_layers < 1 || n_layers > kPoolLayersMax) return hipErrorInvalidValue;
