@@ -82,7 +82,16 @@ int main(void) {
     CHECK(ssba_forward_gated_ex(&d, fake, fake, NULL, (int32_t*)fake, ib, fake, sb, fake, NULL) == SSBA_ERR_ARG);
     d.tile = 16;
     CHECK(ssba_pool_keys_ex(&d, fake, fake, (size_t)1 << 30, NULL) == SSBA_ERR_UNSUPPORTED);
+    CHECK(ssba_rope_pool_keys_ex(&d, fake, fake, fake, fake, 0.f, fake, (size_t)1 << 30, NULL) ==
+          SSBA_ERR_UNSUPPORTED);
     d.tile = 8;
+    /* the rotary forms */
+    CHECK(ssba_rope_pool_keys_ex(&d, fake, fake, fake, fake, 0.f, fake, sb - 1, NULL) == SSBA_ERR_WORKSPACE);
+    CHECK(ssba_rope_pool_keys_ex(&d, fake, fake, NULL, fake, 0.f, fake, sb, NULL) == SSBA_ERR_ARG);
+    CHECK(ssba_forward_topk_rope_ex(&d, fake, fake, fake, fake, fake, 0.f, (int32_t*)fake, ib - 1, fake, sb, fake,
+                                    NULL) == SSBA_ERR_WORKSPACE);
+    CHECK(ssba_forward_topk_rope_ex(&d, fake, fake, fake, fake, fake, 1.0f / 0.0f, (int32_t*)fake, ib, fake, sb,
+                                    fake, NULL) == SSBA_ERR_ARG);
   }
   CHECK(ssba_forward_kernel(&d, 7) == NULL);
 

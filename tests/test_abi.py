@@ -353,3 +353,30 @@ def test_split_fused_launches_checked_before_launch(lib):
     assert _lib.forward_gated(d, fake, fake, fake, fake, fake, fake, None, ib, sb - 1) == W
     bad = _desc(keep=0)
     assert _lib.pool_keys(bad, fake, fake, None, sb) == A
+
+
+def test_rope_calls_checked_before_launch(lib):
+    """ssba_rope_pool_keys_ex and ssba_forward_topk_rope_ex reject
+    unsupported shapes, missing or misaligned buffers, short workspaces and a
+    non-finite frequency base before anything is launched."""
+    fake = 0x100000
+    d = _desc()
+    ib, sb = _lib.workspace_size(d)
+    U, A, W = _lib.SSBA_ERR_UNSUPPORTED, _lib.SSBA_ERR_ARG, _lib.SSBA_ERR_WORKSPACE
+    for other in (_desc(tile=16), _desc(gate=_lib.GATE_TOPK_SHARED), _desc(dtype=_lib.DT_F32)):
+        assert _lib.rope_pool_keys(other, fake, fake, fake, fake, 0.0, fake, None, 1 << 30) == U
+        assert _lib.forward_topk_rope(other, fake, fake, fake, fake, fake, 0.0, fake, fake, fake, None,
+                                      1 << 30, 1 << 30) == U
+    for i in range(4):   # q, k, q_rope, k_rope in turn missing
+        ptrs = [fake] * 4
+        ptrs[i] = None
+        assert _lib.rope_pool_keys(d, *ptrs, 0.0, fake, None, sb) == A
+        ptrs[i] = fake + 8
+        assert _lib.rope_pool_keys(d, *ptrs, 0.0, fake, None, sb) == A
+    assert _lib.rope_pool_keys(d, fake, fake, fake, fake, 0.0, fake, None, sb - 1) == W
+    for theta in (float("nan"), float("inf"), -float("inf")):
+        assert _lib.rope_pool_keys(d, fake, fake, fake, fake, theta, fake, None, sb) == A
+        assert _lib.forward_topk_rope(d, fake, fake, fake, fake, fake, theta, fake, fake, fake, None, ib, sb) == A
+    assert _lib.forward_topk_rope(d, fake, fake, fake, fake, fake, 0.0, fake, fake, fake, None, ib - 1, sb) == W
+    assert _lib.forward_topk_rope(d, fake, fake, None, fake, fake, 0.0, fake, fake, fake, None, ib, sb) == A
+    assert _lib.forward_topk_rope(d, fake, fake, fake, None, fake, 0.0, fake, fake, fake, None, ib, sb) == A
