@@ -38,7 +38,11 @@ ssba_forward_gated_ex on the pooled key sums the step's pooling launch left
 in the scratch: its flops per launch over its average launch time (HIP
 events on the stream it runs on).  roofline_ungated gives the same for the
 attention kernel as ssba_forward launches it (index read, no gate), and
-ms_pool the pooling launch alone.  `traffic` is the HBM traffic per launch
+ms_pool the pooling launch alone.  ms_step_rope times Algorithm 1 in full,
+its rotary step included (ssba_forward_topk_rope_ex: the rotary pre-pass,
+which writes the rotated Q and K and pools the rotated keys, then the gated
+attention on them), and ms_rope_pool / gbs_rope_pool that pre-pass alone
+against its compulsory bytes.  `traffic` is the HBM traffic per launch
 measured with rocprofv3 counters (FETCH_SIZE and WRITE_SIZE, scaled by what
 the same counters read for a plain copy of known size), reported only while
 the kernel's sources still hash to the values the counters were taken on.
@@ -124,6 +128,12 @@ def measured_traffic(kernel: str, workload: str):
     if not m or m["sha"] != sources_sha(kernel):
         return None
     return m["fetch_kib"] * 1024 * m["fetch_factor"] + m["write_kib"] * 1024 * m["write_factor"]
+
+
+def rope_bytes(w) -> int:
+    """Compulsory bytes of the rotary pre-pass: Q and K read, rotated Q and K
+    written, the pooled key sums written (bf16 tensors, fp64 sums)."""
+    return 4 * w.batch * w.heads * w.seq_len * w.head_dim * 2 + w.batch * w.heads * w.n_tiles * w.head_dim * 8
 
 
 def pairs_per_bh(w, keep=None) -> int:
@@ -216,6 +226,19 @@ class Runner:
         """The step's gated attention launch alone (ssba_forward_gated_ex), on
         the pooled key sums the last step or run_pool left in the scratch."""
         self.ssba.forward_gated(self.q, self.k, self.v, self.desc, self.index, self.scratch, self.out)
+
+    def run_rope_step(self):
+        """Algorithm 1 in full, rotary step included (ssba_forward_topk_rope_ex)."""
+        if not hasattr(self, "q_rope"):
+            self.q_rope, self.k_rope = self.torch.empty_like(self.q), self.torch.empty_like(self.k)
+        self.ssba.forward_topk_rope(self.q, self.k, self.v, self.desc, q_rope=self.q_rope, k_rope=self.k_rope,
+                                    index=self.index, scratch=self.scratch, out=self.out)
+
+    def run_rope_pool(self):
+        """Its rotary pre-pass alone (ssba_rope_pool_keys_ex)."""
+        if not hasattr(self, "q_rope"):
+            self.q_rope, self.k_rope = self.torch.empty_like(self.q), self.torch.empty_like(self.k)
+        self.ssba.rope_pool_keys(self.q, self.k, self.desc, self.scratch, q_rope=self.q_rope, k_rope=self.k_rope)
 
     def timed_steps(self, steps: int):
         """Whole steps (index + forward) back to back: wall ms and event ms per step."""
@@ -339,7 +362,7 @@ def measure(w, steps: int, warmup: int, dense_steps: int, graph: bool = True, se
     for _ in range(3):
         r.run_dense()
     fused = r.fused()
-    spans = {"two": [], "idx": [], "fwd": [], "dense": [], "gated": [], "pool": []}
+    spans = {"two": [], "idx": [], "fwd": [], "dense": [], "gated": [], "pool": [], "rope": [], "rope_pool": []}
     for _ in range(REPEATS):
         spans["two"].append(r._span(r.step_two_calls, steps))
         spans["idx"].append(r._span(r.run_index, steps))
@@ -348,10 +371,14 @@ def measure(w, steps: int, warmup: int, dense_steps: int, graph: bool = True, se
         if fused:
             spans["pool"].append(r._span(r.run_pool, steps))
             spans["gated"].append(r._span(r.run_gated, steps))
+            spans["rope"].append(r._span(r.run_rope_step, steps))
+            spans["rope_pool"].append(r._span(r.run_rope_pool, steps))
     two_ms, idx_ms, fwd_ms, dense_ms = (statistics.median(spans[key])
                                         for key in ("two", "idx", "fwd", "dense"))
     gated_ms = statistics.median(spans["gated"]) if fused else None
     pool_ms = statistics.median(spans["pool"]) if fused else None
+    rope_ms = statistics.median(spans["rope"]) if fused else None
+    rope_pool_ms = statistics.median(spans["rope_pool"]) if fused else None
     cold_step_ms = r.cold_ms(r.step)
     cold_fwd_ms = r.cold_ms(r.run_fwd)
     graph_ms = None
@@ -368,7 +395,8 @@ def measure(w, steps: int, warmup: int, dense_steps: int, graph: bool = True, se
     return r, {
         "ms_step_wall": wall_ms, "ms_step_eager": step_ms, "ms_step_graph": graph_ms,
         "ms_step": best_ms, "ms_step_two_calls": two_ms, "ms_index": idx_ms, "ms_fwd": fwd_ms,
-        "ms_dense": dense_ms, "ms_gated": gated_ms, "ms_pool": pool_ms, "ms_step_cold": cold_step_ms,
+        "ms_dense": dense_ms, "ms_gated": gated_ms, "ms_pool": pool_ms, "ms_step_rope": rope_ms,
+        "ms_rope_pool": rope_pool_ms, "ms_step_cold": cold_step_ms,
         "ms_fwd_cold": cold_fwd_ms, "gflop": f / 1e9, "gflop_dense": flops(w, dense=True) / 1e9,
         "tflops_fwd": f / (fwd_ms * 1e-3) / 1e12,
         "tflops_step": f / (best_ms * 1e-3) / 1e12,
@@ -717,6 +745,9 @@ def main():
         "ms_fwd": round(m["ms_fwd"], 5), "ms_index": round(m["ms_index"], 5),
         "ms_gated": None if m["ms_gated"] is None else round(m["ms_gated"], 5),
         "ms_pool": None if m["ms_pool"] is None else round(m["ms_pool"], 5),
+        "ms_step_rope": None if m["ms_step_rope"] is None else round(m["ms_step_rope"], 5),
+        "ms_rope_pool": None if m["ms_rope_pool"] is None else round(m["ms_rope_pool"], 5),
+        "gbs_rope_pool": None if m["ms_rope_pool"] is None else round(rope_bytes(w) / (m["ms_rope_pool"] * 1e-3) / 1e9, 1),
         "ms_dense": round(m["ms_dense"], 5), "ms_step_wall": round(m["ms_step_wall"], 5),
         "ms_step_eager": round(m["ms_step_eager"], 5),
         "ms_step_two_calls": round(m["ms_step_two_calls"], 5),
