@@ -123,23 +123,24 @@ __device__ __forceinline__ uint32_t bf16_bits_rne(double x) {
 }
 
 // Rotary pre-pass of the fused call (Algorithm 1, first step; 2-D axial
-// reading): one workgroup per image block (t, h, b) rotates the block's Q
-// and K rows, writes them to q_out / k_out, and pools the rotated keys like
-// k_pool; text workgroups copy their 64 text rows unchanged.  Channels
-// [0, D/2) turn with the token's row, [D/2, D) with its column; pair i of a
-// half (channels 2i, 2i + 1) by pos * inv_freq[i]; (a, b) ->
-// (a cos - b sin, a sin + b cos) in fp64 with every product rounded, then
-// rounded to bf16.  The block's 8 rows and 8 columns give 2 * 8 * D/4
-// (cos, sin) pairs, one or two per thread.
+// reading).  Per (batch, head) the workgroups are: one per image block for K
+// (rotate the block's K rows, write them, pool the rotated keys like
+// k_pool), one per image block for Q (rotate and write), and one per 64 text
+// rows (copy Q and K unchanged).  Channels [0, D/2) turn with the token's
+// row, [D/2, D) with its column; pair i of a half (channels 2i, 2i + 1) by
+// pos * inv_freq[i]; (a, b) -> (a cos - b sin, a sin + b cos) in fp64 with
+// every product rounded, then rounded to bf16.  The block's 8 rows and 8
+// columns give 2 * 8 * D/4 (cos, sin) pairs, computed while the block's rows
+// are being read.
 template <int D>
 __global__ void __launch_bounds__(256) k_rope_pool_keys(RopeArgs r) {
   constexpr int P = D / 4;            // pairs per half
   constexpr int VPR = D / 8;          // 16-byte pieces per row
-  constexpr int PER = 64 * VPR / 256; // pieces per thread per tensor
+  constexpr int PER = 64 * VPR / 256; // pieces per thread
   __shared__ double cs[2][8][P][2];   // [row / column][index][pair][cos, sin]
   __shared__ uint4 stage[64 * VPR];   // rotated K of the block, [slot][piece]
   const IndexArgs& a = r.a;
-  const int groups = a.n_tiles + r.n_text_groups;
+  const int groups = 2 * a.n_tiles + r.n_text_groups;
   const int id = blockIdx.x, nbh = a.batch * a.heads;
   int bh, g;
   if ((nbh & 7) == 0) {   // whole heads per XCD, as the attention kernel maps them
@@ -152,13 +153,13 @@ __global__ void __launch_bounds__(256) k_rope_pool_keys(RopeArgs r) {
   }
   const int b = bh / a.heads, h = bh - b * a.heads;
   const int64_t base = (int64_t)b * a.sb + (int64_t)h * a.sh;
-  const uint16_t* qin = static_cast<const uint16_t*>(a.q) + base;
-  const uint16_t* kin = static_cast<const uint16_t*>(a.k) + base;
-  uint16_t* qout = static_cast<uint16_t*>(r.q_out) + base;
-  uint16_t* kout = static_cast<uint16_t*>(r.k_out) + base;
   const int tid = threadIdx.x;
-  if (g >= a.n_tiles) {   // text rows: copied
-    const int row0 = 64 * (g - a.n_tiles);
+  if (g >= 2 * a.n_tiles) {   // text rows: copied
+    const uint16_t* qin = static_cast<const uint16_t*>(a.q) + base;
+    const uint16_t* kin = static_cast<const uint16_t*>(a.k) + base;
+    uint16_t* qout = static_cast<uint16_t*>(r.q_out) + base;
+    uint16_t* kout = static_cast<uint16_t*>(r.k_out) + base;
+    const int row0 = 64 * (g - 2 * a.n_tiles);
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int idx = tid + 256 * u, slot = idx / VPR, part = idx % VPR, row = row0 + slot;
@@ -170,7 +171,19 @@ __global__ void __launch_bounds__(256) k_rope_pool_keys(RopeArgs r) {
     }
     return;
   }
-  const int t = g, W = a.f.grid_w;
+  const bool is_k = g < a.n_tiles;
+  const int t = is_k ? g : g - a.n_tiles, W = a.f.grid_w;
+  const uint16_t* in = static_cast<const uint16_t*>(is_k ? a.k : a.q) + base;
+  uint16_t* out = static_cast<uint16_t*>(is_k ? r.k_out : r.q_out) + base;
+  // The block's rows, requested first.
+  uint4 v[PER];
+  int64_t off[PER];
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int idx = tid + 256 * u, slot = idx / VPR, part = idx % VPR;
+    off[u] = (int64_t)frame_row(a.f, t, slot) * a.st + part * 8;
+    v[u] = *reinterpret_cast<const uint4*>(in + off[u]);
+  }
   // (cos, sin) of the block's rows and columns.
   for (int k = tid; k < 2 * 8 * P; k += 256) {
     const int axis = k / (8 * P), j = (k / P) % 8, i = k % P;
@@ -186,28 +199,24 @@ __global__ void __launch_bounds__(256) k_rope_pool_keys(RopeArgs r) {
 #pragma unroll
   for (int u = 0; u < PER; ++u) {
     const int idx = tid + 256 * u, slot = idx / VPR, part = idx % VPR;
-    const int64_t off = (int64_t)frame_row(a.f, t, slot) * a.st + part * 8;
     const int c0 = 8 * part, axis = c0 / (D / 2), i0 = (c0 % (D / 2)) / 2;
     const int j = axis == 0 ? slot / 8 : slot % 8;
+    const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+    uint32_t o[4];
 #pragma unroll
-    for (int tensor = 0; tensor < 2; ++tensor) {
-      const uint4 in = *reinterpret_cast<const uint4*>((tensor ? kin : qin) + off);
-      const uint32_t w[4] = {in.x, in.y, in.z, in.w};
-      uint32_t o[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {   // word e holds channels c0 + 2e (low half) and c0 + 2e + 1
-        const double x0 = (double)__uint_as_float(w[e] << 16);
-        const double x1 = (double)__uint_as_float(w[e] & 0xFFFF0000u);
-        const double c = cs[axis][j][i0 + e][0], sn = cs[axis][j][i0 + e][1];
-        const double y0 = __dsub_rn(__dmul_rn(x0, c), __dmul_rn(x1, sn));
-        const double y1 = __dadd_rn(__dmul_rn(x0, sn), __dmul_rn(x1, c));
-        o[e] = bf16_bits_rne(y0) | (bf16_bits_rne(y1) << 16);
-      }
-      const uint4 ov = make_uint4(o[0], o[1], o[2], o[3]);
-      *reinterpret_cast<uint4*>((tensor ? kout : qout) + off) = ov;
-      if (tensor) stage[idx] = ov;
+    for (int e = 0; e < 4; ++e) {   // word e holds channels c0 + 2e (low half) and c0 + 2e + 1
+      const double x0 = (double)__uint_as_float(w[e] << 16);
+      const double x1 = (double)__uint_as_float(w[e] & 0xFFFF0000u);
+      const double c = cs[axis][j][i0 + e][0], sn = cs[axis][j][i0 + e][1];
+      const double y0 = __dsub_rn(__dmul_rn(x0, c), __dmul_rn(x1, sn));
+      const double y1 = __dadd_rn(__dmul_rn(x0, sn), __dmul_rn(x1, c));
+      o[e] = bf16_bits_rne(y0) | (bf16_bits_rne(y1) << 16);
     }
+    const uint4 ov = make_uint4(o[0], o[1], o[2], o[3]);
+    *reinterpret_cast<uint4*>(out + off[u]) = ov;
+    if (is_k) stage[idx] = ov;
   }
+  if (!is_k) return;
   __syncthreads();
   // Pooled rotated keys: thread c adds channel c over the slots in order.
   if (tid < D) {
@@ -500,7 +509,7 @@ hipError_t launch_rope_pool_keys(const RopeArgs& r, hipStream_t s) {
   const IndexArgs& a = r.a;
   if (a.f.tile_log2 != 3 || (a.head_dim != 64 && a.head_dim != 128) || r.n_text_groups < 0)
     return hipErrorInvalidValue;   // 8x8 blocks (the gated attention kernel)
-  dim3 grid((a.n_tiles + r.n_text_groups) * a.heads * a.batch), block(256);
+  dim3 grid((2 * a.n_tiles + r.n_text_groups) * a.heads * a.batch), block(256);
   if (a.head_dim == 64) hipLaunchKernelGGL((k_rope_pool_keys<64>), grid, block, 0, s, r);
   else hipLaunchKernelGGL((k_rope_pool_keys<128>), grid, block, 0, s, r);
   return hipGetLastError();
