@@ -212,9 +212,10 @@ ssba_status ssba_forward_train_ex(const ssba_desc* d, const void* q, const void*
                                   void* hip_stream);
 
 /* Device bytes of the scratch ssba_backward needs (256-byte aligned buffer):
- * fp32 [B][H][T] twice (the log-sum-exp in log2 units and rowsum(dO * O)) and
- * a 64-bit mask of kept blocks per query block, [B][H][T_b]; each region
- * rounded up to 256 bytes. */
+ * fp32 [B][H][T] twice (the log-sum-exp in log2 units and rowsum(dO * O)), a
+ * 64-bit mask of kept blocks per query block, [B][H][T_b], and the order in
+ * which the key-side kernel takes the key blocks, int32 [B][H][T_b]; each
+ * region rounded up to 256 bytes. */
 ssba_status ssba_backward_workspace_size(const ssba_desc* d, size_t* scratch_bytes);
 
 /* Backward of the SSBA attention with the gate held fixed (the kept lists

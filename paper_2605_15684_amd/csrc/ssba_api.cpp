@@ -125,10 +125,11 @@ size_t scratch_bytes_of(const ssba_desc* d, const Shape& s) {
 }
 
 // Backward scratch: lse2 and D ([B][H][T] fp32 each), then each query
-// block's kept blocks as a 64-bit mask ([B][H][T_b]); every region 256-byte
+// block's kept blocks as a 64-bit mask ([B][H][T_b]), then the key blocks in
+// the key-side kernel's order (int32 [B][H][T_b]); every region 256-byte
 // aligned.
 struct BwdScratch {
-  size_t lse2, delta, kmask, total;
+  size_t lse2, delta, kmask, korder, total;
 };
 
 BwdScratch bwd_scratch(const ssba_desc* d, const Shape& s) {
@@ -138,7 +139,8 @@ BwdScratch bwd_scratch(const ssba_desc* d, const Shape& s) {
   w.lse2 = 0;
   w.delta = up(4 * rows);
   w.kmask = w.delta + up(4 * rows);
-  w.total = w.kmask + up((size_t)8 * d->batch * d->heads * s.n_tiles);
+  w.korder = w.kmask + up((size_t)8 * d->batch * d->heads * s.n_tiles);
+  w.total = w.korder + up((size_t)4 * d->batch * d->heads * s.n_tiles);
   return w;
 }
 
@@ -484,6 +486,7 @@ ssba_status ssba_backward_ex(const ssba_desc* d, const void* q, const void* k, c
   a.lse2 = reinterpret_cast<float*>(base + w.lse2);
   a.delta = reinterpret_cast<float*>(base + w.delta);
   a.kmask = reinterpret_cast<unsigned long long*>(base + w.kmask);
+  a.korder = reinterpret_cast<int32_t*>(base + w.korder);
   a.index = index;
   a.sb = s.sb;
   a.sh = s.sh;

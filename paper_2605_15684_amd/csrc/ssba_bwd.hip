@@ -204,11 +204,56 @@ __device__ __forceinline__ void copy_rowvals(const __amdgpu_buffer_rsrc_t& rs, c
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)dst, 4, 4u * (unsigned)row, 0, 0, 0);
 }
 
+// The key-side kernel's order of work for head bh: its key blocks sorted by
+// the number of query blocks that keep them (descending, ties by block id),
+// written to korder[bh][rank].  A key block's workgroup loops over exactly
+// those query blocks, so with the groups dispatched in this order the longest
+// start first and the short ones fill the slots that free up (longest-first
+// list scheduling); the results do not depend on the order.  All four waves
+// of one workgroup take part (the call is workgroup-uniform); `cnt` is 64
+// ints of LDS that no wave reads or writes meanwhile.  The lists come from
+// the index, complete before the backward starts.
+__device__ __forceinline__ void write_key_order(const BwdArgs& a, int bh, int w, int lane, int* cnt) {
+  const int tb = a.n_tiles;   // <= 64
+  const int32_t* head = a.index + (int64_t)bh * tb * (tb + 1);
+  constexpr int LPW = 16;     // lists per wave: wave w takes lists w, w + 4, ...
+  // Every load is issued before any is used: lane i holds list i's length,
+  // lane e entry e of each of the wave's lists.
+  const int len = lane < tb ? head[(int64_t)lane * (tb + 1)] : 0;
+  int e[LPW];
+#pragma unroll
+  for (int u = 0; u < LPW; ++u) {
+    const int i = w + 4 * u;
+    e[u] = i < tb && lane < tb ? head[(int64_t)i * (tb + 1) + 1 + lane] : -1;
+  }
+  if (w == 0) cnt[lane] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < LPW; ++u) {
+    const int i = w + 4 * u;
+    const int n = i < tb ? min(max(__builtin_amdgcn_readlane(len, i), 0), tb) : 0;
+    if (lane < n && (unsigned)e[u] < (unsigned)tb) atomicAdd(&cnt[e[u]], 1);
+  }
+  __syncthreads();
+  if (w == 0 && lane < tb) {
+    const int mine = cnt[lane];
+    int rank = 0;
+    for (int j = 0; j < tb; ++j) {
+      const int c = cnt[j];
+      rank += (c > mine || (c == mine && j < lane)) ? 1 : 0;
+    }
+    a.korder[(int64_t)bh * tb + rank] = lane;
+  }
+}
+
 // Workgroup -> (b, h, group): every (b, h) owns n_text_groups text groups and
 // n_tiles << QL image groups (one per chunk of every block); with a head count
 // divisible by 8 each XCD (hardware ids go round-robin over the 8) gets whole
 // heads, text groups first.
-template <int QL>
+// With RANK_MAJOR the image groups of an XCD's heads are interleaved (group
+// 0 of every head, then group 1, ...), so that the launch dispatches group g
+// of all heads before group g + 1 of any.
+template <int QL, bool RANK_MAJOR = false>
 __device__ __forceinline__ void group_of(const BwdArgs& a, int& bh, int& r) {
   const int n_img = a.n_tiles << QL;
   const int bid = blockIdx.x, nbh = a.batch * a.heads, gpb = a.n_text_groups + n_img;
@@ -220,9 +265,16 @@ __device__ __forceinline__ void group_of(const BwdArgs& a, int& bh, int& r) {
       r = s % nt;
     } else {
       const int s2 = s - hpx * nt;
-      bh = xcd * hpx + s2 / n_img;
-      r = nt + s2 % n_img;
+      bh = xcd * hpx + (RANK_MAJOR ? s2 % hpx : s2 / n_img);
+      r = nt + (RANK_MAJOR ? s2 / hpx : s2 % n_img);
     }
+  } else if (RANK_MAJOR && bid >= nbh * a.n_text_groups) {
+    const int s2 = bid - nbh * a.n_text_groups;
+    bh = s2 % nbh;
+    r = a.n_text_groups + s2 / nbh;
+  } else if (RANK_MAJOR) {
+    bh = bid / a.n_text_groups;
+    r = bid - bh * a.n_text_groups;
   } else {
     bh = bid / gpb;
     r = bid - bh * gpb;
@@ -458,17 +510,21 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
       for (int j = 0; j < 16; ++j) xo[(16 * db + j) * 64 + lane] = acc[db][j];
   }
   __syncthreads();
-  if (sk == 1 || qrow < 0) return;
-  u16* orow = static_cast<u16*>(a.dq) + off + (int64_t)qrow * st;
+  if (sk == 0 && qrow >= 0) {
+    u16* orow = static_cast<u16*>(a.dq) + off + (int64_t)qrow * st;
 #pragma unroll
-  for (int db = 0; db < NDB; ++db)
+    for (int db = 0; db < NDB; ++db)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      float v[4];
+      for (int j = 0; j < 4; ++j) {
+        float v[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = (acc[db][4 * j + e] + xo[(16 * db + 4 * j + e) * 64 + lane]) * a.scale;
-      *reinterpret_cast<uint2*>(orow + 32 * db + 8 * j + 4 * hw) = make_uint2(pack2(v[0], v[1]), pack2(v[2], v[3]));
-    }
+        for (int e = 0; e < 4; ++e) v[e] = (acc[db][4 * j + e] + xo[(16 * db + 4 * j + e) * 64 + lane]) * a.scale;
+        *reinterpret_cast<uint2*>(orow + 32 * db + 8 * j + 4 * hw) = make_uint2(pack2(v[0], v[1]), pack2(v[2], v[3]));
+      }
+  }
+  // The first image group of each head also orders the key-side work (the dO
+  // stage is free after the chunk loop).
+  if (!text_group && g == 0) write_key_order(a, bh, w, lane, reinterpret_cast<int*>(gstage));
 }
 
 // --------------------------------------------------------------------------
@@ -506,7 +562,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
   __shared__ __attribute__((aligned(16))) char kst[2 * NKS * 1024];
   __shared__ __attribute__((aligned(16))) char vst[2 * NKS * 1024];
   int bh, r;
-  group_of<QL>(a, bh, r);
+  group_of<QL, true>(a, bh, r);
   const int b = bh / a.heads, h = bh - b * a.heads;
   const int64_t off = (int64_t)b * a.sb + (int64_t)h * a.sh;
   const u16* qbase = static_cast<const u16*>(a.q) + off;
@@ -520,8 +576,11 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(D == 6
   const int tb = a.n_tiles;
 
   const bool text_group = r < a.n_text_groups;
-  const int g = r - a.n_text_groups, kj = g >> QL, kq = g & (GPB - 1);
+  const int g = r - a.n_text_groups, kq = g & (GPB - 1);
   const uint64_t mask_i = lane < tb ? a.kmask[(int64_t)bh * tb + lane] : 0ull;   // query block i's kept set
+  // Image group g serves the key block of rank g >> QL in the head's
+  // longest-first order (written by the query-side kernel).
+  const int kj = text_group ? 0 : a.korder[(int64_t)bh * tb + (g >> QL)];
 
   // This lane's key row.  An image group is chunk kq of key block kj.
   int krow;

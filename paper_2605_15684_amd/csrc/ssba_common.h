@@ -149,6 +149,7 @@ struct BwdArgs {
   float* delta;          // [B][H][T] scratch: rowsum(dO * O)
   const int32_t* index;  // [B][H][T_b][1 + T_b]
   unsigned long long* kmask;  // [B][H][T_b] scratch: kept blocks of each query block as bits
+  int32_t* korder;            // [B][H][T_b] scratch: key blocks in the key-side kernel's order
   int64_t sb, sh, st;
   int batch, heads, seq, n_tiles, n_text_groups;
   Frame f;

@@ -178,7 +178,8 @@ int main() {
     size_t bsb = 0;
     CHECK(ssba_backward_workspace_size(&d, &bsb) == SSBA_OK);
     const size_t up = (4 * 16 * 4096 + 255) / 256 * 256;
-    CHECK(bsb == 2 * up + (8 * 16 * 64 + 255) / 256 * 256);
+    const size_t mask_bytes = (8 * 16 * 64 + 255) / 256 * 256;
+    CHECK(bsb == 2 * up + mask_bytes + (4 * 16 * 64 + 255) / 256 * 256);
     Buffers b(tensor, ib, bsb + 256);
     // 256-byte aligned scratch inside the vector
     char* raw = reinterpret_cast<char*>(b.scratch.data());
@@ -192,6 +193,7 @@ int main() {
                            b.q.data(), b.k.data(), b.v.data(), scr, bsb, nullptr) == SSBA_OK);
     CHECK(stub_calls().size() == 1 && stub_calls()[0].scratch == scr);
     CHECK(stub_calls()[0].flags == static_cast<char*>(scr) + 2 * up);
+    CHECK(stub_calls()[0].out == static_cast<char*>(scr) + 2 * up + mask_bytes);
   }
 
   // ---- layer stack: slices, offsets, skipped layers, index cache ----------

@@ -71,7 +71,7 @@ hipError_t launch_attn_mfma_layers(const AttnLayers& p, int n_layers, int, int, 
   return hipSuccess;
 }
 hipError_t launch_backward(const BwdArgs& a, int, hipStream_t) {
-  stub_calls().push_back({"backward", a.index, a.lse2, a.kmask, a.dq, 0, a.f.sy, a.f.sx, 0});
+  stub_calls().push_back({"backward", a.index, a.lse2, a.kmask, a.korder, 0, a.f.sy, a.f.sx, 0});
   return hipSuccess;
 }
 

@@ -8,7 +8,7 @@ struct StubCall {
   const void* index;      // index read or written (the layer pre-pass: the keys pooled)
   const void* scratch;    // pooled sums (q for the gates, k for the attention and the layer pre-pass), backward lse2
   const void* flags;      // status flags (gates) / kept-block masks (backward)
-  const void* out;        // attention output
+  const void* out;        // attention output (backward: the key-side order)
   int keep, sy, sx, gated;
 };
 

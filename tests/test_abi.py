@@ -269,7 +269,7 @@ def test_backward_workspace_size(lib):
     d = _desc(batch=2, heads=3, n_text=10)
     rows = 2 * 3 * (10 + 4096)
     up = lambda x: (x + 255) // 256 * 256
-    assert _lib.backward_workspace_size(d) == 2 * up(4 * rows) + up(8 * 2 * 3 * 64)
+    assert _lib.backward_workspace_size(d) == 2 * up(4 * rows) + up(8 * 2 * 3 * 64) + up(4 * 2 * 3 * 64)
 
 
 def test_probe_rejects_bad_arguments(lib):

@@ -162,3 +162,54 @@ def test_forward_train_output_equals_forward():
     o2, _ = ssba.forward_train(qg, kg, vg, index, desc)
     torch.cuda.synchronize()
     assert torch.equal(o1, o2)
+
+
+def _key_order_region(desc_w, scratch, tb):
+    """The backward scratch's key-order region (int32 [B][H][T_b]), located by
+    the layout ssba_backward_workspace_size documents."""
+    up = lambda x: (x + 255) // 256 * 256
+    bh = desc_w.batch * desc_w.heads
+    off = 2 * up(4 * bh * desc_w.seq_len) + up(8 * bh * tb)
+    raw = scratch.view(torch.uint8)[off:off + 4 * bh * tb].cpu()
+    return raw.view(torch.int32).numpy().reshape(bh, tb)
+
+
+@pytest.mark.parametrize("w,truncate", [
+    (preset("grid64", heads=2), False),
+    (preset("grid64", heads=2), True),
+    (workload_from(batch=2, heads=1, grid_h=64, grid_w=48, head_dim=64, tile=16, keep=5, shift=(3, -7),
+                   n_text=77), True),
+], ids=["grid64", "grid64-ragged-lists", "16x16-text-ragged-lists"])
+def test_key_side_order_is_longest_first(w, truncate):
+    """The key-side kernel takes each head's key blocks in descending order of
+    the number of lists that keep them, ties by block id; the order is left
+    in the scratch.  With ragged lists (list i cut to 1 + i mod keep
+    entries) the counts see only each list's first n entries.  A second run
+    on a fresh scratch gives the same gradients."""
+    from paper_2605_15684_amd import _lib, ssba
+    (_, _, _), (qg, kg, vg) = inputs(w)
+    desc = gpu_desc(w, qg)
+    index, _ = ssba.build_index(qg, kg, desc)
+    tb = (w.grid_h // w.tile) * (w.grid_w // w.tile)
+    if truncate:
+        host = index.cpu().numpy().reshape(-1, tb, tb + 1).copy()
+        host[:, :, 0] = 1 + np.arange(tb)[None, :] % w.keep
+        index = torch.from_numpy(host.reshape(index.shape)).to("cuda")
+    out, lse = ssba.forward_train(qg, kg, vg, index, desc)
+    dout = _dout(w).to("cuda")
+    sb = _lib.backward_workspace_size(desc)
+    scratch = torch.full(((sb + 7) // 8,), -1.0, dtype=torch.float64, device="cuda")
+    first = ssba.backward(qg, kg, vg, out, dout, lse, index, desc, scratch=scratch)
+    torch.cuda.synchronize()
+    got = _key_order_region(w, scratch, tb)
+    lists = index.cpu().numpy().reshape(-1, tb, tb + 1)
+    for bh in range(lists.shape[0]):
+        cnt = np.zeros(tb, dtype=np.int64)
+        for i in range(tb):
+            n = min(max(int(lists[bh, i, 0]), 0), tb)
+            np.add.at(cnt, lists[bh, i, 1:1 + n], 1)
+        want = sorted(range(tb), key=lambda j: (-cnt[j], j))
+        assert got[bh].tolist() == want, f"head {bh}"
+    again = ssba.backward(qg, kg, vg, out, dout, lse, index, desc)
+    torch.cuda.synchronize()
+    assert all(torch.equal(x, y) for x, y in zip(first, again))
