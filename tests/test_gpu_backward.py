@@ -128,8 +128,10 @@ def test_backward_grid128_full_size_sampled_head():
 
 
 def test_backward_text_full_size_sampled_heads():
-    w = preset("grid64_text", batch=1, heads=4)
-    heads = [(0, 0), (0, 3)]
+    # 16 heads: two per XCD, so the key side's rank-major numbering
+    # interleaves heads, after the text groups.
+    w = preset("grid64_text", batch=1, heads=16)
+    heads = [(0, 0), (0, 9)]
     got, ref = _run(w, heads=heads)
     _check(got, ref, heads)
 
