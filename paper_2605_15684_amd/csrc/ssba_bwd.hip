@@ -250,9 +250,10 @@ __device__ __forceinline__ void write_key_order(const BwdArgs& a, int bh, int w,
 // n_tiles << QL image groups (one per chunk of every block); with a head count
 // divisible by 8 each XCD (hardware ids go round-robin over the 8) gets whole
 // heads, text groups first.
-// With RANK_MAJOR the image groups of an XCD's heads are interleaved (group
-// 0 of every head, then group 1, ...), so that the launch dispatches group g
-// of all heads before group g + 1 of any.
+// With RANK_MAJOR the image groups are numbered group-major across heads
+// (group 0 of every head, then group 1, ...; within each XCD's heads when
+// the head count divides by 8, across all heads otherwise), so that the
+// launch dispatches group g of those heads before group g + 1 of any.
 template <int QL, bool RANK_MAJOR = false>
 __device__ __forceinline__ void group_of(const BwdArgs& a, int& bh, int& r) {
   const int n_img = a.n_tiles << QL;
