@@ -111,6 +111,38 @@ def test_backward_small_against_oracle(w):
     _check(got, ref, [(b, h) for b in range(w.batch) for h in range(w.heads)])
 
 
+RAGGED = [
+    workload_from(batch=1, heads=2, grid_h=32, grid_w=32, head_dim=64, tile=8, keep=6, shift=(4, 4), n_text=20),
+    workload_from(batch=2, heads=1, grid_h=48, grid_w=40, head_dim=128, tile=8, keep=7, shift=(3, 5)),
+    workload_from(batch=1, heads=2, grid_h=48, grid_w=64, head_dim=128, tile=16, keep=5, shift=(-8, 5),
+                  n_text=13),
+]
+
+
+@pytest.mark.parametrize("w", RAGGED, ids=lambda w: f"{w.grid_h}x{w.grid_w}-D{w.head_dim}-b{w.tile}-t{w.n_text}")
+def test_backward_ragged_lists_against_oracle(w):
+    """Lists of different lengths (query block i keeps the first 1 + (i mod
+    keep) blocks of its top-k list, so the key blocks are kept unevenly and
+    the key side's longest-first order differs from block order): the
+    training forward and the backward on that index, on every row, against
+    the oracle on the same index."""
+    from paper_2605_15684_amd import ssba
+    (q, k, v), (qg, kg, vg) = inputs(w)
+    desc = gpu_desc(w, qg)
+    idx = oracle_index(w, q, k).copy()
+    tb = w.n_tiles
+    lists = idx.reshape(-1, tb, tb + 1)
+    lists[:, :, 0] = 1 + np.arange(tb)[None, :] % w.keep
+    index = torch.from_numpy(idx).to("cuda")
+    out, lse = ssba.forward_train(qg, kg, vg, index, desc)
+    dout = _dout(w)
+    dq, dk, dv = ssba.backward(qg, kg, vg, out, dout.to("cuda"), lse, index, desc)
+    torch.cuda.synchronize()
+    ref = O.attention_backward(to64(q), to64(k), to64(v), to64(dout), idx, **oracle_kw(w))
+    heads = [(b, h) for b in range(w.batch) for h in range(w.heads)]
+    _check((dq, dk, dv, lse), ref + (_lse_bound(w, q, k, idx, heads),), heads)
+
+
 def test_backward_full_size_sampled_heads():
     w = preset("grid64")
     heads = [(0, 0), (0, 7), (0, 15)]
