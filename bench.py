@@ -94,10 +94,10 @@ MEASURED_TRAFFIC = {
     ("k_haar_dwt<unsigned short, 3>", "haar512"): {"sha": "02be9c317bd1aa8b", "fetch_kib": 131115.0,
                                                   "write_kib": 344064.0, "fetch_factor": 1.9998,
                                                   "write_factor": 1.0},
-    ("k_attn_mfma<64, 3, false, true>", "grid64"): {"sha": "af5c2141dcd67036", "fetch_kib": 12668.0,
+    ("k_attn_mfma<64, 3, false, true>", "grid64"): {"sha": "5c3b7efa87c23894", "fetch_kib": 12668.0,
                                                     "write_kib": 8456.0, "fetch_factor": 1.99984,
                                                     "write_factor": 1.0},
-    ("k_attn_mfma<64, 3, false, false>", "grid64"): {"sha": "af5c2141dcd67036", "fetch_kib": 12554.7,
+    ("k_attn_mfma<64, 3, false, false>", "grid64"): {"sha": "5c3b7efa87c23894", "fetch_kib": 12554.8,
                                                      "write_kib": 8192.0, "fetch_factor": 1.99984,
                                                      "write_factor": 1.0},
 }

@@ -142,8 +142,10 @@ ssba_status ssba_build_index_ex(const ssba_desc* d, const void* q, const void* k
  * the image rows are the layer output of Algorithm 1's return step.
  * bf16: products and accumulation in fp32 (MFMA), probabilities rounded to
  * bf16 before the value product, output rounded to bf16.  f32: fp32 throughout.
- * `index` must come from ssba_build_index with the same grid/tile/shift
- * (counts in 0..T_b, ids in 0..T_b-1; other contents are undefined behaviour). */
+ * `index` must come from ssba_build_index with the same grid/tile/shift, or
+ * hold lists of the same layout (counts in 0..T_b, ids in 0..T_b-1; other
+ * contents are undefined behaviour).  A query that sees no key (an empty
+ * list and no text tokens) gets a row of zeros. */
 ssba_status ssba_forward(const ssba_desc* d, const void* q, const void* k, const void* v,
                          const int32_t* index, void* o, void* hip_stream);
 
