@@ -514,7 +514,7 @@ ssba_status ssba_layers_workspace_size(const ssba_desc* d, int n_layers, size_t*
                                        size_t* scratch_bytes) {
   if (!d || n_layers < 1) return SSBA_ERR_ARG;
   ssba_desc base = *d;
-  if (is_topk(base.gate)) base.keep = 1;   // per-layer keeps are checked by the driver
+  if (is_topk(base.gate)) base.keep = 1;   // per-layer keeps are checked by the layer driver
   Shape s;
   const ssba_status st = check_desc(&base, &s);
   if (st != SSBA_OK) return st;
