@@ -89,6 +89,9 @@ def _check(got, ref, heads):
 
 
 CASES = [
+    # one and two blocks per head (the key-side order over a single block)
+    workload_from(batch=1, heads=2, grid_h=8, grid_w=8, head_dim=64, tile=8, keep=1, shift=(4, 4)),
+    workload_from(batch=2, heads=1, grid_h=8, grid_w=16, head_dim=128, tile=8, keep=1, shift=(-4, 4), n_text=5),
     workload_from(batch=1, heads=2, grid_h=16, grid_w=16, head_dim=64, tile=8, keep=2, shift=(4, 4)),
     workload_from(batch=1, heads=2, grid_h=32, grid_w=32, head_dim=64, tile=8, keep=5, shift=(-4, -4), n_text=13),
     workload_from(batch=2, heads=1, grid_h=48, grid_w=40, head_dim=64, tile=8, keep=7, shift=(3, 5), n_text=77),
