@@ -263,6 +263,15 @@ TOPK_CASES = [
     preset("grid128", heads=2),                                  # 16x16 blocks: two-call route
     preset("tiny"),                                              # fp32: two-call route
 ]
+# Few blocks per head in the gated kernel: one block, two blocks both kept
+# (with text), sixteen blocks all kept.
+FEW_BLOCKS = [
+    workload_from(batch=1, heads=2, grid_h=8, grid_w=8, head_dim=64, tile=8, keep=1, shift=(4, 4)),
+    workload_from(batch=2, heads=1, grid_h=8, grid_w=16, head_dim=128, tile=8, keep=2, shift=(-4, 4),
+                  n_text=5),
+    workload_from(batch=1, heads=2, grid_h=32, grid_w=32, head_dim=64, tile=8, keep=16, shift=(4, 4)),
+]
+TOPK_CASES += FEW_BLOCKS
 
 
 @pytest.mark.parametrize("w", TOPK_CASES, ids=_ids)
@@ -283,7 +292,7 @@ def test_forward_topk_equals_build_index_then_forward(w):
     assert torch.equal(out1, out2)
 
 
-@pytest.mark.parametrize("w", TOPK_CASES[:5], ids=_ids)
+@pytest.mark.parametrize("w", TOPK_CASES[:5] + FEW_BLOCKS, ids=_ids)
 def test_pool_keys_then_forward_gated_equals_forward_topk(w):
     """The fused form's two launches called one at a time give the fused
     call's index rows, status flags and output bit for bit; the index is the
@@ -301,6 +310,21 @@ def test_pool_keys_then_forward_gated_equals_forward_topk(w):
     assert torch.equal(index1, index2) and torch.equal(out1, out2)
     assert ssba.read_status(desc, scratch2) == 0
     assert np.array_equal(index2.cpu().numpy(), oracle_index(w, q, k))
+
+
+@pytest.mark.parametrize("w", FEW_BLOCKS, ids=_ids)
+def test_forward_topk_few_blocks_against_oracle(w):
+    """The fused call with one, two and sixteen blocks per head: index bit
+    exact and every output row within tolerance of the oracle."""
+    from paper_2605_15684_amd import ssba
+    (q, k, v), (qg, kg, vg) = inputs(w)
+    index, _, out = ssba.forward_topk(qg, kg, vg, gpu_desc(w, qg))
+    torch.cuda.synchronize()
+    want_idx = oracle_index(w, q, k)
+    assert np.array_equal(index.cpu().numpy(), want_idx)
+    ref = O.attention(to64(q), to64(k), to64(v), want_idx, **oracle_kw(w))
+    err = float(np.abs(out.float().cpu().double().numpy() - ref).max())
+    assert err <= tol(w), f"max-abs {err:.3e}"
 
 
 def test_forward_topk_full_size_against_oracle():
